@@ -1,0 +1,25 @@
+"""Plain, slow CPU oracle of the windowed-attention chunk step (UnStep, arXiv 2609.32518).
+
+TEST INFRASTRUCTURE ONLY.  Only ``tests/``, ``__graft_entry__.smoke()`` and the
+``cpu_baseline`` leg of ``bench.py`` may import or run anything under
+``oracle/``; the library itself never does, and the oracle shares no code with
+it (only the seeded input generators in ``synth`` serve both).
+
+What it defines, each in fp64 unless the paper fixes a precision:
+
+* ``tables``   -- the per-chunk rotary cos/sin tables (Appendix A.6: cached fp32
+                  coefficients keyed by start frame and grid).
+* ``rope``     -- the pair rotation of Appendix A.6 under the rounding contract
+                  "bf16 in, fp32 math, bf16 out", plus the ideal fp64 rotation.
+* ``kvcache``  -- the sink + sliding-window KV cache with host-held indices
+                  (Section 3.1, Section 3.3, Appendix A.3, Appendix A.6).
+* ``attention`` -- exact softmax attention of the chunk's queries over the
+                  retained keys, and a brute-force full-timeline masked version.
+
+Where the paper is silent, the reading taken is stated in the function that
+depends on it.  Parity of attention against the paper itself is unpinned (the
+paper prints no tensor values for this path); it is pinned by brute force,
+closed forms and invariants in ``tests/test_oracle_*.py``.
+"""
+from . import numerics, tables, rope, kvcache, attention  # noqa: F401
+from .kvcache import OracleError  # noqa: F401
