@@ -1,0 +1,200 @@
+/*
+ * unstep.h -- C ABI of the windowed-attention chunk step of a causal video DiT
+ * (UnStep, arXiv 2609.32518), for one AMD MI355X (gfx950).
+ *
+ * One self-attention step for a chunk of C latent frames (Section 3.1, Section 3.3,
+ * Appendix A.3 and A.6 of the paper):
+ *   1. rotate the chunk's queries and keys with cached fp32 cos/sin tables (3D RoPE);
+ *   2. write the rotated keys and the values into a sink + ring-buffer KV cache whose
+ *      positions are held on the host;
+ *   3. run softmax attention of the chunk's queries over the retained keys: the sink
+ *      frames older than the window, the W frames before the chunk, and the chunk.
+ *
+ * Conventions shared by every entry point:
+ *   - bf16 tensors are passed as `const void*` / `void*` holding IEEE bfloat16 values;
+ *     fp32 tensors as `float*`.  Device pointers are caller-owned (this library never
+ *     allocates, frees or reads device memory on the step path) and must be 16-byte
+ *     aligned; head_dim (the innermost axis) has stride 1.
+ *   - Token order inside a chunk is frame-major, then grid row, then grid column:
+ *     token n = (i*grid_h + r)*grid_w + c for chunk frame i, row r, column c.
+ *   - N = n_frames * T, T = grid_h * grid_w tokens per latent frame.
+ *   - Functions taking `hip_stream` enqueue their kernels on that stream (a
+ *     hipStream_t; NULL = the default stream) and return without synchronising,
+ *     except unstep_rope_tables, which waits for its upload (it runs once per
+ *     (start frame, grid), off the step path).
+ *   - Every function returns UNSTEP_OK or a negative unstep_status and never aborts;
+ *     unstep_last_error() then describes the failure.  All argument and state checks
+ *     happen before any work is enqueued; a failed call changes no state.
+ *   - A cache handle is not thread-safe; distinct handles are independent.
+ *   - Only head_dim == 128 is supported (the model's 12 heads of width 128, App. A.6).
+ */
+#ifndef UNSTEP_H
+#define UNSTEP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  UNSTEP_OK = 0,
+  UNSTEP_E_NULL = -1,   /* a required pointer is NULL                                   */
+  UNSTEP_E_SHAPE = -2,  /* unsupported or inconsistent sizes (head_dim != 128, empty...) */
+  UNSTEP_E_RANGE = -3,  /* frame index / window / chunk outside what the cache can hold  */
+  UNSTEP_E_STATE = -4,  /* cache state forbids the call (gap, evicted or missing frame)  */
+  UNSTEP_E_HIP = -5,    /* the HIP runtime reported an error (message from HIP)          */
+  UNSTEP_E_ALIGN = -6   /* a pointer is not 16-byte aligned or a stride not a multiple of 8 */
+} unstep_status;
+
+#define UNSTEP_HEAD_DIM 128
+#define UNSTEP_MAX_SEGMENTS 4
+
+/* Library version, major*10000 + minor*100 + patch. */
+int unstep_version(void);
+
+/* Message describing the last failed call on this thread ("" if none).  The string is
+ * owned by the library and valid until the next call on the same thread. */
+const char* unstep_last_error(void);
+
+/* ---------------------------------------------------------------------------------
+ * KV cache handle: host-held positions (Section 3.1 and Appendix A.6: the positions
+ * depend only on token counts, so they live on the CPU and no call reads the GPU).
+ *
+ * Slots: S sink slots hold frames 0..S-1; R ring slots hold every later frame f at
+ * slot S + (f - S) mod R (the sink + sliding-window cache of Section 3.3 / App. A.3,
+ * evicting whole latent frames).  Token t of the frame in slot s is cache row s*T + t.
+ * ------------------------------------------------------------------------------- */
+typedef struct unstep_cache unstep_cache;
+
+/* Create a handle over caller-owned device buffers k_cache, v_cache, each bf16
+ * [batch, n_heads, (sink_frames + ring_frames) * grid_h * grid_w, head_dim], which the
+ * caller keeps alive until unstep_cache_destroy.  The handle starts empty (no frame
+ * stored).  Touches no device memory.  Errors: E_NULL (out, k_cache, v_cache),
+ * E_SHAPE (head_dim != 128, batch/n_heads/grid < 1, sink_frames < 0, ring_frames < 1,
+ * sizes beyond 2^31 rows), E_ALIGN. */
+int unstep_cache_create(unstep_cache** out, int32_t batch, int32_t n_heads, int32_t head_dim,
+                        int32_t grid_h, int32_t grid_w, int32_t sink_frames, int32_t ring_frames,
+                        void* k_cache, void* v_cache);
+
+/* Free the host state (never the device buffers).  NULL is accepted. */
+int unstep_cache_destroy(unstep_cache* c);
+
+/* Host copy of the index state: frame_of_slot[S + R] receives the latent frame stored
+ * in each slot (-1 = never written); *newest (optional) the newest frame stored
+ * (-1 = none).  Errors: E_NULL. */
+int unstep_cache_frame_map(const unstep_cache* c, int32_t* frame_of_slot, int32_t* newest);
+
+/* Record frames [start_frame, start_frame + n_frames) as stored without touching device
+ * memory, exactly as unstep_kv_append would update the positions (same checks).  For
+ * callers that fill the K/V buffers by other means, e.g. restoring a snapshot (the K/V
+ * buffers plus the frame map are the whole cache state).  Errors: as the index checks
+ * of unstep_kv_append (E_NULL, E_SHAPE, E_RANGE, E_STATE). */
+int unstep_cache_advance(unstep_cache* c, int32_t start_frame, int32_t n_frames);
+
+/* Retained keys of the chunk [start_frame, start_frame + n_frames) with a window of
+ * window_frames prior frames: frames [0, min(S, lo)) then [lo, start_frame + n_frames),
+ * lo = max(0, start_frame - window_frames), in that order (the sinks, the window, the
+ * chunk; Section 3.3).  Written as maximal runs of consecutive cache rows:
+ * seg_row0[i], seg_len[i] for i < *n_seg (at most UNSTEP_MAX_SEGMENTS).
+ * Errors: E_NULL, E_SHAPE (n_frames < 1), E_RANGE (negative frame or window; more
+ * ring frames retained than the ring holds), E_STATE (a retained frame is not in the
+ * cache: never appended or evicted). */
+int unstep_window_segments(const unstep_cache* c, int32_t start_frame, int32_t n_frames,
+                           int32_t window_frames, int32_t* seg_row0, int32_t* seg_len,
+                           int32_t* n_seg);
+
+/* ---------------------------------------------------------------------------------
+ * Rotary tables (Appendix A.6: fp32 cos/sin per token and coordinate pair, shared by
+ * all heads, cached per (start latent frame, grid size)).
+ *
+ * Pair j = 0..head_dim/2-1 belongs to the temporal axis for j < d_t/2, to the grid
+ * row axis for the next d_h/2 pairs and to the column axis for the last d_w/2, with
+ * d_h = d_w = 2*(head_dim/6) and d_t = head_dim - d_h - d_w (22/21/21 pairs at 128).
+ * Pair j with ladder step k on an axis of d_a dims turns by angle p * w,
+ * w = 1 / pow(theta, 2k/d_a), p = the token's absolute frame index, grid row or grid
+ * column.  Angle, pow, cos and sin are evaluated in double precision with the C
+ * library and rounded once to float.
+ * ------------------------------------------------------------------------------- */
+
+/* Host variant: writes cos_out, sin_out (host float [N, head_dim/2]).  Touches no GPU.
+ * Errors: E_NULL, E_SHAPE (head_dim not 128, sizes < 1), E_RANGE (start_frame < 0,
+ * theta <= 1). */
+int unstep_rope_tables_host(int32_t start_frame, int32_t n_frames, int32_t grid_h, int32_t grid_w,
+                            int32_t head_dim, double theta, float* cos_out, float* sin_out);
+
+/* Device variant: the same tables written to device buffers cos_out, sin_out (float
+ * [N, head_dim/2]) through hip_stream; returns after the upload completed.
+ * Errors: as the host variant, plus E_ALIGN and E_HIP. */
+int unstep_rope_tables(int32_t start_frame, int32_t n_frames, int32_t grid_h, int32_t grid_w,
+                       int32_t head_dim, double theta, float* cos_out, float* sin_out,
+                       void* hip_stream);
+
+/* ---------------------------------------------------------------------------------
+ * Fused RoPE + KV append (Section 3.1 and Appendix A.6; one bandwidth-bound pass).
+ *
+ * For every chunk token n, head h, pair j (x_e = x[2j], x_o = x[2j+1], c/s the table
+ * entries of token n, pair j):  y_e = x_e*c - x_o*s,  y_o = x_e*s + x_o*c, each
+ * product and the sum/difference an IEEE fp32 operation rounded to nearest-even (no
+ * fused multiply-add), the result rounded to bf16 nearest-even.
+ *   q_rot[b, n, h, :] = rotate(q[b, n, h, :])             (skipped if q == NULL)
+ *   K-cache row of token n = rotate(k[b, n, h, :]);  V-cache row of token n = v (bits)
+ * q, k, v: bf16 [batch, N, n_heads, 128] at element strides tok_stride (between tokens)
+ * and head_stride (between heads); batch stride N*tok_stride.  q_rot: bf16 contiguous
+ * [batch, N, n_heads, 128].  cos_t, sin_t: device float [N, 64] from unstep_rope_tables
+ * for the same start frame and grid.
+ *
+ * Index update (host): the chunk may start at most one frame after the newest stored
+ * frame; re-appending stored frames overwrites them in place without advancing the
+ * positions (repeated denoising calls, App. A.6); new frames evict the ring slot's
+ * previous frame.  Errors: E_NULL (c, k, v, cos_t, sin_t; q_rot when q != NULL),
+ * E_SHAPE (n_frames < 1, strides too small), E_ALIGN, E_RANGE (start_frame < 0; more
+ * ring frames than the ring holds), E_STATE (gap after the newest frame; a re-appended
+ * frame was evicted), E_HIP.  On error nothing is enqueued and the state is unchanged. */
+int unstep_kv_append(unstep_cache* c, int32_t start_frame, int32_t n_frames,
+                     const void* q, const void* k, const void* v,
+                     int64_t tok_stride, int64_t head_stride,
+                     const float* cos_t, const float* sin_t,
+                     void* q_rot, void* hip_stream);
+
+/* ---------------------------------------------------------------------------------
+ * Windowed block-causal attention (Sections 3.1 and 3.3; Appendix A.3).
+ *
+ * out[b, n, h, :] = sum_m softmax_m(scale * <q_rot[b, n, h, :], K_m>) V_m over the
+ * retained keys m of unstep_window_segments (every query of the chunk sees every
+ * retained key, the chunk's own included).  bf16 MFMA products, fp32 accumulation and
+ * fp32 online softmax; out is bf16 [batch, N, n_heads, 128] contiguous.  lse
+ * (optional, NULL to skip): float [batch, n_heads, N], the natural-log
+ * log-sum-exp of the scaled scores.  softmax_scale <= 0 selects 1/sqrt(128).
+ *
+ * workspace (optional): device scratch for splitting the key range over several
+ * work-groups; unstep_attn_workspace_size gives the bytes used for this call.  With
+ * workspace == NULL or workspace_bytes smaller than that, the call runs unsplit (same
+ * results up to fp32 summation order, possibly slower).  The size depends only on the
+ * shapes (batch, heads, chunk tokens, retained key count), not on what is stored, so it
+ * can be queried before the chunk is appended.
+ * Errors: those of unstep_window_segments, plus E_NULL (q_rot, out), E_ALIGN, E_HIP;
+ * unstep_attn_workspace_size: E_NULL, E_SHAPE, E_RANGE (argument checks only). */
+int unstep_attn_workspace_size(const unstep_cache* c, int32_t start_frame, int32_t n_frames,
+                               int32_t window_frames, size_t* bytes);
+
+int unstep_window_attn(const unstep_cache* c, int32_t start_frame, int32_t n_frames,
+                       int32_t window_frames, const void* q_rot, void* out, float* lse,
+                       float softmax_scale, void* workspace, size_t workspace_bytes,
+                       void* hip_stream);
+
+/* ---------------------------------------------------------------------------------
+ * One whole chunk step: unstep_kv_append followed by unstep_window_attn on the same
+ * stream (q must not be NULL).  All checks of both halves run before anything is
+ * enqueued.  Errors: the union of both. */
+int unstep_step(unstep_cache* c, int32_t start_frame, int32_t n_frames, int32_t window_frames,
+                const void* q, const void* k, const void* v, int64_t tok_stride, int64_t head_stride,
+                const float* cos_t, const float* sin_t, void* q_rot, void* out, float* lse,
+                float softmax_scale, void* workspace, size_t workspace_bytes, void* hip_stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* UNSTEP_H */

@@ -1,0 +1,242 @@
+"""Python binding of libunstep.so: the windowed-attention chunk step of a causal video
+DiT (UnStep, arXiv 2609.32518) on one AMD MI355X.
+
+Argument marshalling only: every step of the path runs in the library's HIP kernels.
+PyTorch provides device memory (tensors) and the stream; the library's C ABI
+(include/unstep.h) takes raw pointers.  The binding has the same names as the ABI:
+``unstep_rope_tables``, ``unstep_kv_append``, ``unstep_window_attn``, ``unstep_step``
+as methods/functions below, plus a ``Cache`` handle.
+
+Importing this package loads libunstep.so and raises if it is missing: there is no
+fallback path.  Build it with ``python paper_2609_32518_amd/build.py``.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, List, Optional, Tuple
+
+import torch
+
+HEAD_DIM = 128
+MAX_SEGMENTS = 4
+
+OK, E_NULL, E_SHAPE, E_RANGE, E_STATE, E_HIP, E_ALIGN = 0, -1, -2, -3, -4, -5, -6
+STATUS_NAMES = {OK: "OK", E_NULL: "E_NULL", E_SHAPE: "E_SHAPE", E_RANGE: "E_RANGE", E_STATE: "E_STATE",
+                E_HIP: "E_HIP", E_ALIGN: "E_ALIGN"}
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libunstep.so")
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build it with `python paper_2609_32518_amd/build.py` "
+                      "(there is no non-HIP fallback)")
+lib = ctypes.CDLL(LIB_PATH)
+
+_i32, _i64, _f32, _f64 = ctypes.c_int32, ctypes.c_int64, ctypes.c_float, ctypes.c_double
+_vp, _sz = ctypes.c_void_p, ctypes.c_size_t
+_pi32 = ctypes.POINTER(ctypes.c_int32)
+_pf32 = ctypes.POINTER(ctypes.c_float)
+
+# exported symbol -> (restype, argtypes); mirrors include/unstep.h
+SIGNATURES = {
+    "unstep_version": (ctypes.c_int, []),
+    "unstep_last_error": (ctypes.c_char_p, []),
+    "unstep_cache_create": (ctypes.c_int, [ctypes.POINTER(_vp), _i32, _i32, _i32, _i32, _i32, _i32, _i32, _vp, _vp]),
+    "unstep_cache_destroy": (ctypes.c_int, [_vp]),
+    "unstep_cache_frame_map": (ctypes.c_int, [_vp, _pi32, _pi32]),
+    "unstep_cache_advance": (ctypes.c_int, [_vp, _i32, _i32]),
+    "unstep_window_segments": (ctypes.c_int, [_vp, _i32, _i32, _i32, _pi32, _pi32, _pi32]),
+    "unstep_rope_tables_host": (ctypes.c_int, [_i32, _i32, _i32, _i32, _i32, _f64, _pf32, _pf32]),
+    "unstep_rope_tables": (ctypes.c_int, [_i32, _i32, _i32, _i32, _i32, _f64, _vp, _vp, _vp]),
+    "unstep_kv_append": (ctypes.c_int, [_vp, _i32, _i32, _vp, _vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp]),
+    "unstep_attn_workspace_size": (ctypes.c_int, [_vp, _i32, _i32, _i32, ctypes.POINTER(_sz)]),
+    "unstep_window_attn": (ctypes.c_int, [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _f32, _vp, _sz, _vp]),
+    "unstep_step": (ctypes.c_int, [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp, _vp,
+                                   _f32, _vp, _sz, _vp]),
+}
+for _name, (_res, _args) in SIGNATURES.items():
+    _fn = getattr(lib, _name)
+    _fn.restype = _res
+    _fn.argtypes = _args
+
+
+class UnstepError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{STATUS_NAMES.get(code, code)}: {msg}")
+        self.code = code
+
+
+def _check(rc: int) -> None:
+    if rc != OK:
+        raise UnstepError(rc, lib.unstep_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream: Optional[torch.cuda.Stream]) -> int:
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return s.cuda_stream
+
+
+def version() -> int:
+    return lib.unstep_version()
+
+
+def unstep_rope_tables_host(start_frame: int, n_frames: int, grid_h: int, grid_w: int,
+                            head_dim: int = HEAD_DIM, theta: float = 10000.0):
+    """Host (numpy float32) cos/sin tables [N, head_dim/2] built by the library."""
+    import numpy as np
+    n = n_frames * grid_h * grid_w
+    c = np.empty((n, head_dim // 2), dtype=np.float32)
+    s = np.empty_like(c)
+    _check(lib.unstep_rope_tables_host(start_frame, n_frames, grid_h, grid_w, head_dim, theta,
+                                       c.ctypes.data_as(_pf32), s.ctypes.data_as(_pf32)))
+    return c, s
+
+
+def unstep_rope_tables(start_frame: int, n_frames: int, grid_h: int, grid_w: int, head_dim: int = HEAD_DIM,
+                       theta: float = 10000.0, device="cuda", stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Device cos/sin tables [N, head_dim/2] float32 (blocking upload)."""
+    n = n_frames * grid_h * grid_w
+    c = torch.empty((n, head_dim // 2), dtype=torch.float32, device=device)
+    s = torch.empty_like(c)
+    _check(lib.unstep_rope_tables(start_frame, n_frames, grid_h, grid_w, head_dim, theta, c.data_ptr(),
+                                  s.data_ptr(), _stream(stream)))
+    return c, s
+
+
+class RopeTableCache:
+    """Tables keyed by (start frame, n_frames, grid_h, grid_w, theta), built once and reused
+    by every layer and denoising call of that chunk (Appendix A.6)."""
+
+    def __init__(self, device="cuda"):
+        self.device = device
+        self._tables: Dict[tuple, Tuple[torch.Tensor, torch.Tensor]] = {}
+
+    def get(self, start_frame: int, n_frames: int, grid_h: int, grid_w: int, theta: float = 10000.0):
+        key = (start_frame, n_frames, grid_h, grid_w, theta)
+        if key not in self._tables:
+            self._tables[key] = unstep_rope_tables(start_frame, n_frames, grid_h, grid_w, HEAD_DIM, theta,
+                                                   self.device)
+        return self._tables[key]
+
+
+class Cache:
+    """KV cache of one attention layer: device K/V buffers bf16 [B, H, (S+R)*T, 128] owned by
+    this object, host-held positions owned by the library handle."""
+
+    def __init__(self, batch: int, n_heads: int, grid_h: int, grid_w: int, sink_frames: int, ring_frames: int,
+                 device="cuda", k_cache: Optional[torch.Tensor] = None, v_cache: Optional[torch.Tensor] = None,
+                 head_dim: int = HEAD_DIM):
+        self.B, self.H, self.grid_h, self.grid_w = batch, n_heads, grid_h, grid_w
+        self.S, self.R = sink_frames, ring_frames
+        self.T = grid_h * grid_w
+        self.slots = (sink_frames + ring_frames) * self.T
+        shape = (batch, n_heads, self.slots, head_dim)
+        self.k = k_cache if k_cache is not None else torch.zeros(shape, dtype=torch.bfloat16, device=device)
+        self.v = v_cache if v_cache is not None else torch.zeros(shape, dtype=torch.bfloat16, device=device)
+        h = _vp()
+        _check(lib.unstep_cache_create(ctypes.byref(h), batch, n_heads, head_dim, grid_h, grid_w, sink_frames,
+                                       ring_frames, self.k.data_ptr(), self.v.data_ptr()))
+        self.handle = h
+        self._ws: Optional[torch.Tensor] = None
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h is not None and h.value:
+            lib.unstep_cache_destroy(h)
+            self.handle = None
+
+    # -- host index state ------------------------------------------------------------
+    def frame_map(self) -> Tuple[List[int], int]:
+        fm = (ctypes.c_int32 * (self.S + self.R))()
+        newest = ctypes.c_int32()
+        _check(lib.unstep_cache_frame_map(self.handle, fm, ctypes.byref(newest)))
+        return list(fm), newest.value
+
+    def advance(self, start_frame: int, n_frames: int) -> None:
+        """Record frames as stored without writing device memory (snapshot restore)."""
+        _check(lib.unstep_cache_advance(self.handle, start_frame, n_frames))
+
+    def segments(self, start_frame: int, n_frames: int, window_frames: int) -> List[Tuple[int, int]]:
+        r0 = (ctypes.c_int32 * MAX_SEGMENTS)()
+        ln = (ctypes.c_int32 * MAX_SEGMENTS)()
+        n = ctypes.c_int32()
+        _check(lib.unstep_window_segments(self.handle, start_frame, n_frames, window_frames, r0, ln,
+                                          ctypes.byref(n)))
+        return [(r0[i], ln[i]) for i in range(n.value)]
+
+    def workspace_bytes(self, start_frame: int, n_frames: int, window_frames: int) -> int:
+        b = _sz()
+        _check(lib.unstep_attn_workspace_size(self.handle, start_frame, n_frames, window_frames, ctypes.byref(b)))
+        return b.value
+
+    def workspace(self, start_frame: int, n_frames: int, window_frames: int) -> Optional[torch.Tensor]:
+        """Device scratch for split-key attention, grown on demand and kept."""
+        need = self.workspace_bytes(start_frame, n_frames, window_frames)
+        if need == 0:
+            return None
+        if self._ws is None or self._ws.numel() < need:
+            self._ws = torch.empty(need, dtype=torch.uint8, device=self.k.device)
+        return self._ws
+
+    # -- step path --------------------------------------------------------------------
+    @staticmethod
+    def _strides(x: torch.Tensor) -> Tuple[int, int]:
+        if x.dtype != torch.bfloat16 or x.dim() != 4 or x.shape[-1] != HEAD_DIM or x.stride(-1) != 1:
+            raise ValueError("q/k/v must be bf16 [B, N, H, 128] with unit stride on the last axis")
+        return x.stride(1), x.stride(2)
+
+    def unstep_kv_append(self, start_frame: int, n_frames: int, q: Optional[torch.Tensor], k: torch.Tensor,
+                         v: torch.Tensor, cos_t: torch.Tensor, sin_t: torch.Tensor,
+                         q_rot: Optional[torch.Tensor] = None, stream=None) -> Optional[torch.Tensor]:
+        ts, hs = self._strides(k)
+        if self._strides(v) != (ts, hs) or (q is not None and self._strides(q) != (ts, hs)):
+            raise ValueError("q, k, v must share strides")
+        if q is not None and q_rot is None:
+            q_rot = torch.empty((self.B, n_frames * self.T, self.H, HEAD_DIM), dtype=torch.bfloat16,
+                                device=k.device)
+        _check(lib.unstep_kv_append(self.handle, start_frame, n_frames, _ptr(q), k.data_ptr(), v.data_ptr(), ts, hs,
+                                    cos_t.data_ptr(), sin_t.data_ptr(), _ptr(q_rot), _stream(stream)))
+        return q_rot
+
+    def unstep_window_attn(self, start_frame: int, n_frames: int, window_frames: int, q_rot: torch.Tensor,
+                           out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                           softmax_scale: float = 0.0, workspace: Optional[torch.Tensor] = None,
+                           use_split: bool = True, stream=None) -> torch.Tensor:
+        if out is None:
+            out = torch.empty_like(q_rot)
+        if workspace is None and use_split:
+            workspace = self.workspace(start_frame, n_frames, window_frames)
+        ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+        _check(lib.unstep_window_attn(self.handle, start_frame, n_frames, window_frames, q_rot.data_ptr(),
+                                      out.data_ptr(), _ptr(lse), softmax_scale, _ptr(workspace), ws_bytes,
+                                      _stream(stream)))
+        return out
+
+    def unstep_step(self, start_frame: int, n_frames: int, window_frames: int, q: torch.Tensor, k: torch.Tensor,
+                    v: torch.Tensor, cos_t: torch.Tensor, sin_t: torch.Tensor, q_rot: Optional[torch.Tensor] = None,
+                    out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
+                    softmax_scale: float = 0.0, workspace: Optional[torch.Tensor] = None, use_split: bool = True,
+                    stream=None) -> torch.Tensor:
+        ts, hs = self._strides(q)
+        if self._strides(k) != (ts, hs) or self._strides(v) != (ts, hs):
+            raise ValueError("q, k, v must share strides")
+        N = n_frames * self.T
+        if q_rot is None:
+            q_rot = torch.empty((self.B, N, self.H, HEAD_DIM), dtype=torch.bfloat16, device=q.device)
+        if out is None:
+            out = torch.empty((self.B, N, self.H, HEAD_DIM), dtype=torch.bfloat16, device=q.device)
+        if workspace is None and use_split:
+            workspace = self._step_workspace(start_frame, n_frames, window_frames)
+        ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+        _check(lib.unstep_step(self.handle, start_frame, n_frames, window_frames, q.data_ptr(), k.data_ptr(),
+                               v.data_ptr(), ts, hs, cos_t.data_ptr(), sin_t.data_ptr(), q_rot.data_ptr(),
+                               out.data_ptr(), _ptr(lse), softmax_scale, _ptr(workspace), ws_bytes,
+                               _stream(stream)))
+        return out
+
+    def _step_workspace(self, start_frame: int, n_frames: int, window_frames: int) -> Optional[torch.Tensor]:
+        return self.workspace(start_frame, n_frames, window_frames)

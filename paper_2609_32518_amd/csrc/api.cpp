@@ -1,0 +1,320 @@
+// C ABI of the windowed-attention chunk step (declared in include/unstep.h).
+//
+// Every entry point validates its arguments and the host-held cache state first and
+// only then enqueues kernels, so a failing call leaves no trace on the GPU or in the
+// handle.  Nothing here reads device memory or synchronises, except
+// unstep_rope_tables, which waits for its table upload.
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "cache_index.hpp"
+#include "kernels.hpp"
+#include "rope_tables.hpp"
+#include "unstep.h"
+
+struct unstep_cache {
+  unstep::CacheIndex idx;
+  int32_t B, H, D, grid_h, grid_w;
+  int32_t slots;
+  uint16_t* k;
+  uint16_t* v;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+int ok() {
+  g_err.clear();
+  return UNSTEP_OK;
+}
+
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int fail_msg(int code, const char* where, const std::string& why) {
+  return fail(code, "%s: %s", where, why.c_str());
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+int check_table_args(const char* where, int32_t f0, int32_t F, int32_t gh, int32_t gw, int32_t D,
+                     double theta, const void* c, const void* s) {
+  if (!c || !s) return fail(UNSTEP_E_NULL, "%s: cos_out/sin_out is NULL", where);
+  if (D != UNSTEP_HEAD_DIM) return fail(UNSTEP_E_SHAPE, "%s: head_dim %d unsupported (need 128)", where, D);
+  if (F < 1 || gh < 1 || gw < 1) return fail(UNSTEP_E_SHAPE, "%s: n_frames, grid_h, grid_w must be >= 1", where);
+  if (int64_t(F) * gh * gw > (int64_t(1) << 31) / 64)
+    return fail(UNSTEP_E_SHAPE, "%s: table too large", where);
+  if (f0 < 0 || int64_t(f0) + F > INT32_MAX) return fail(UNSTEP_E_RANGE, "%s: bad start_frame", where);
+  if (!(theta > 1.0) || !std::isfinite(theta)) return fail(UNSTEP_E_RANGE, "%s: theta must be > 1", where);
+  return UNSTEP_OK;
+}
+
+struct AppendPlan {
+  unstep::RopeAppendArgs args;
+};
+
+// Validation of an append on index `idx` (which may be a scratch copy).
+int plan_append(const unstep_cache* c, const unstep::CacheIndex& idx, int32_t f0, int32_t C,
+                const void* q, const void* k, const void* v, int64_t tok_stride, int64_t head_stride,
+                const float* cos_t, const float* sin_t, void* q_rot, AppendPlan* plan, const char* where) {
+  if (!c) return fail(UNSTEP_E_NULL, "%s: cache handle is NULL", where);
+  if (!k || !v || !cos_t || !sin_t) return fail(UNSTEP_E_NULL, "%s: k, v, cos_t or sin_t is NULL", where);
+  if (q && !q_rot) return fail(UNSTEP_E_NULL, "%s: q given but q_rot is NULL", where);
+  std::string why;
+  int rc = idx.check_append(f0, C, &why);
+  if (rc != UNSTEP_OK) return fail_msg(rc, where, why);
+  if (head_stride < UNSTEP_HEAD_DIM || tok_stride < int64_t(c->H) * head_stride)
+    return fail(UNSTEP_E_SHAPE, "%s: strides (tok %lld, head %lld) overlap for %d heads of 128", where,
+                (long long)tok_stride, (long long)head_stride, c->H);
+  if ((tok_stride % 8) || (head_stride % 8))
+    return fail(UNSTEP_E_ALIGN, "%s: strides must be multiples of 8 elements", where);
+  if (!aligned16(k) || !aligned16(v) || !aligned16(cos_t) || !aligned16(sin_t) || (q && !aligned16(q)) ||
+      (q_rot && !aligned16(q_rot)))
+    return fail(UNSTEP_E_ALIGN, "%s: pointers must be 16-byte aligned", where);
+  unstep::RopeAppendArgs& a = plan->args;
+  a.q = static_cast<const uint16_t*>(q);
+  a.k = static_cast<const uint16_t*>(k);
+  a.v = static_cast<const uint16_t*>(v);
+  a.tok_stride = tok_stride;
+  a.head_stride = head_stride;
+  a.cos_t = cos_t;
+  a.sin_t = sin_t;
+  a.q_rot = q ? static_cast<uint16_t*>(q_rot) : nullptr;
+  a.k_cache = c->k;
+  a.v_cache = c->v;
+  a.B = c->B;
+  a.H = c->H;
+  a.T = idx.T();
+  a.C = C;
+  a.slots = c->slots;
+  a.f0 = f0;
+  a.S = idx.S();
+  a.R = idx.R();
+  return UNSTEP_OK;
+}
+
+int plan_attn(const unstep_cache* c, const unstep::CacheIndex& idx, int32_t f0, int32_t C, int32_t W,
+              const void* q_rot, void* out, float* lse, float scale, void* workspace, size_t ws_bytes,
+              unstep::AttnArgs* a, const char* where) {
+  if (!c) return fail(UNSTEP_E_NULL, "%s: cache handle is NULL", where);
+  if (!q_rot || !out) return fail(UNSTEP_E_NULL, "%s: q_rot or out is NULL", where);
+  unstep::Segments seg;
+  std::string why;
+  int rc = idx.segments(f0, C, W, &seg, &why);
+  if (rc != UNSTEP_OK) return fail_msg(rc, where, why);
+  if (!aligned16(q_rot) || !aligned16(out) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3u)) ||
+      (workspace && !aligned16(workspace)))
+    return fail(UNSTEP_E_ALIGN, "%s: pointers must be 16-byte aligned", where);
+  const int32_t N = C * idx.T();
+  a->q = static_cast<const uint16_t*>(q_rot);
+  a->k_cache = c->k;
+  a->v_cache = c->v;
+  a->out = static_cast<uint16_t*>(out);
+  a->lse = lse;
+  a->B = c->B;
+  a->N = N;
+  a->H = c->H;
+  a->slots = c->slots;
+  a->n_keys = seg.total();
+  a->n_seg = seg.n;
+  int32_t l = 0;
+  for (int i = 0; i < UNSTEP_MAX_SEGMENTS; ++i) {
+    if (i < seg.n) {
+      a->seg_l0[i] = l;
+      a->seg_row0[i] = seg.row0[i];
+      l += seg.len[i];
+    } else {
+      a->seg_l0[i] = INT32_MAX;
+      a->seg_row0[i] = 0;
+    }
+  }
+  a->seg_l0[UNSTEP_MAX_SEGMENTS] = INT32_MAX;
+  a->scale = scale > 0.f ? scale : 1.0f / std::sqrt(float(UNSTEP_HEAD_DIM));
+  int32_t splits = unstep::attn_choose_splits(c->B, c->H, N, a->n_keys);
+  const size_t need = unstep::attn_workspace_bytes(c->B, c->H, N, splits);
+  if (splits > 1 && (!workspace || ws_bytes < need)) splits = 1;
+  a->splits = splits;
+  if (splits > 1) {
+    const size_t rows = size_t(splits) * c->B * c->H * N;
+    a->part_o = static_cast<float*>(workspace);
+    a->part_ml = static_cast<float*>(workspace) + rows * UNSTEP_HEAD_DIM;
+  } else {
+    a->part_o = nullptr;
+    a->part_ml = nullptr;
+  }
+  return UNSTEP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int unstep_version(void) { return 100; }
+
+const char* unstep_last_error(void) { return g_err.c_str(); }
+
+int unstep_cache_create(unstep_cache** out, int32_t batch, int32_t n_heads, int32_t head_dim, int32_t grid_h,
+                        int32_t grid_w, int32_t sink_frames, int32_t ring_frames, void* k_cache, void* v_cache) {
+  if (!out || !k_cache || !v_cache) return fail(UNSTEP_E_NULL, "unstep_cache_create: NULL argument");
+  if (head_dim != UNSTEP_HEAD_DIM)
+    return fail(UNSTEP_E_SHAPE, "unstep_cache_create: head_dim %d unsupported (need 128)", head_dim);
+  if (batch < 1 || n_heads < 1 || grid_h < 1 || grid_w < 1 || sink_frames < 0 || ring_frames < 1)
+    return fail(UNSTEP_E_SHAPE, "unstep_cache_create: sizes must be >= 1 (sink_frames >= 0)");
+  const int64_t T = int64_t(grid_h) * grid_w;
+  const int64_t slots = (int64_t(sink_frames) + ring_frames) * T;
+  if (slots > INT32_MAX / 2 || int64_t(batch) * n_heads > 65535 || T > INT32_MAX / 64)
+    return fail(UNSTEP_E_SHAPE, "unstep_cache_create: cache too large");
+  if (!aligned16(k_cache) || !aligned16(v_cache))
+    return fail(UNSTEP_E_ALIGN, "unstep_cache_create: cache buffers must be 16-byte aligned");
+  unstep_cache* c = new (std::nothrow) unstep_cache{unstep::CacheIndex(int32_t(T), sink_frames, ring_frames),
+                                                    batch, n_heads, head_dim, grid_h, grid_w, int32_t(slots),
+                                                    static_cast<uint16_t*>(k_cache),
+                                                    static_cast<uint16_t*>(v_cache)};
+  if (!c) return fail(UNSTEP_E_SHAPE, "unstep_cache_create: out of host memory");
+  *out = c;
+  return ok();
+}
+
+int unstep_cache_destroy(unstep_cache* c) {
+  delete c;
+  return ok();
+}
+
+int unstep_cache_frame_map(const unstep_cache* c, int32_t* frame_of_slot, int32_t* newest) {
+  if (!c || !frame_of_slot) return fail(UNSTEP_E_NULL, "unstep_cache_frame_map: NULL argument");
+  const auto& m = c->idx.frame_of_slot();
+  for (size_t i = 0; i < m.size(); ++i) frame_of_slot[i] = m[i];
+  if (newest) *newest = c->idx.newest();
+  return ok();
+}
+
+int unstep_cache_advance(unstep_cache* c, int32_t start_frame, int32_t n_frames) {
+  if (!c) return fail(UNSTEP_E_NULL, "unstep_cache_advance: cache handle is NULL");
+  std::string why;
+  int rc = c->idx.check_append(start_frame, n_frames, &why);
+  if (rc != UNSTEP_OK) return fail_msg(rc, "unstep_cache_advance", why);
+  c->idx.commit_append(start_frame, n_frames);
+  return ok();
+}
+
+int unstep_window_segments(const unstep_cache* c, int32_t start_frame, int32_t n_frames, int32_t window_frames,
+                           int32_t* seg_row0, int32_t* seg_len, int32_t* n_seg) {
+  if (!c || !seg_row0 || !seg_len || !n_seg) return fail(UNSTEP_E_NULL, "unstep_window_segments: NULL argument");
+  unstep::Segments s;
+  std::string why;
+  int rc = c->idx.segments(start_frame, n_frames, window_frames, &s, &why);
+  if (rc != UNSTEP_OK) return fail_msg(rc, "unstep_window_segments", why);
+  for (int i = 0; i < s.n; ++i) {
+    seg_row0[i] = s.row0[i];
+    seg_len[i] = s.len[i];
+  }
+  *n_seg = s.n;
+  return ok();
+}
+
+int unstep_rope_tables_host(int32_t start_frame, int32_t n_frames, int32_t grid_h, int32_t grid_w, int32_t head_dim,
+                            double theta, float* cos_out, float* sin_out) {
+  int rc = check_table_args("unstep_rope_tables_host", start_frame, n_frames, grid_h, grid_w, head_dim, theta,
+                            cos_out, sin_out);
+  if (rc != UNSTEP_OK) return rc;
+  unstep::build_rope_tables(start_frame, n_frames, grid_h, grid_w, head_dim, theta, cos_out, sin_out);
+  return ok();
+}
+
+int unstep_rope_tables(int32_t start_frame, int32_t n_frames, int32_t grid_h, int32_t grid_w, int32_t head_dim,
+                       double theta, float* cos_out, float* sin_out, void* hip_stream) {
+  int rc = check_table_args("unstep_rope_tables", start_frame, n_frames, grid_h, grid_w, head_dim, theta, cos_out,
+                            sin_out);
+  if (rc != UNSTEP_OK) return rc;
+  if (!aligned16(cos_out) || !aligned16(sin_out))
+    return fail(UNSTEP_E_ALIGN, "unstep_rope_tables: pointers must be 16-byte aligned");
+  const size_t n = size_t(n_frames) * grid_h * grid_w * (head_dim / 2);
+  std::vector<float> hc(n), hs(n);
+  unstep::build_rope_tables(start_frame, n_frames, grid_h, grid_w, head_dim, theta, hc.data(), hs.data());
+  hipStream_t st = static_cast<hipStream_t>(hip_stream);
+  hipError_t e = hipMemcpyAsync(cos_out, hc.data(), n * sizeof(float), hipMemcpyHostToDevice, st);
+  if (e == hipSuccess) e = hipMemcpyAsync(sin_out, hs.data(), n * sizeof(float), hipMemcpyHostToDevice, st);
+  if (e == hipSuccess) e = hipStreamSynchronize(st);
+  if (e != hipSuccess) return fail(UNSTEP_E_HIP, "unstep_rope_tables: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int unstep_kv_append(unstep_cache* c, int32_t start_frame, int32_t n_frames, const void* q, const void* k,
+                     const void* v, int64_t tok_stride, int64_t head_stride, const float* cos_t,
+                     const float* sin_t, void* q_rot, void* hip_stream) {
+  if (!c) return fail(UNSTEP_E_NULL, "unstep_kv_append: cache handle is NULL");
+  AppendPlan p;
+  int rc = plan_append(c, c->idx, start_frame, n_frames, q, k, v, tok_stride, head_stride, cos_t, sin_t, q_rot,
+                       &p, "unstep_kv_append");
+  if (rc != UNSTEP_OK) return rc;
+  hipError_t e = unstep::launch_rope_append(p.args, static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return fail(UNSTEP_E_HIP, "unstep_kv_append: %s", hipGetErrorString(e));
+  c->idx.commit_append(start_frame, n_frames);
+  return ok();
+}
+
+int unstep_attn_workspace_size(const unstep_cache* c, int32_t start_frame, int32_t n_frames, int32_t window_frames,
+                               size_t* bytes) {
+  if (!c || !bytes) return fail(UNSTEP_E_NULL, "unstep_attn_workspace_size: NULL argument");
+  int32_t frames = 0;
+  std::string why;
+  int rc = c->idx.retained_count(start_frame, n_frames, window_frames, &frames, &why);
+  if (rc != UNSTEP_OK) return fail_msg(rc, "unstep_attn_workspace_size", why);
+  const int32_t N = n_frames * c->idx.T();
+  const int32_t splits = unstep::attn_choose_splits(c->B, c->H, N, frames * c->idx.T());
+  *bytes = unstep::attn_workspace_bytes(c->B, c->H, N, splits);
+  return ok();
+}
+
+int unstep_window_attn(const unstep_cache* c, int32_t start_frame, int32_t n_frames, int32_t window_frames,
+                       const void* q_rot, void* out, float* lse, float softmax_scale, void* workspace,
+                       size_t workspace_bytes, void* hip_stream) {
+  if (!c) return fail(UNSTEP_E_NULL, "unstep_window_attn: cache handle is NULL");
+  unstep::AttnArgs a;
+  int rc = plan_attn(c, c->idx, start_frame, n_frames, window_frames, q_rot, out, lse, softmax_scale, workspace,
+                     workspace_bytes, &a, "unstep_window_attn");
+  if (rc != UNSTEP_OK) return rc;
+  hipError_t e = unstep::launch_window_attn(a, static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return fail(UNSTEP_E_HIP, "unstep_window_attn: %s", hipGetErrorString(e));
+  return ok();
+}
+
+int unstep_step(unstep_cache* c, int32_t start_frame, int32_t n_frames, int32_t window_frames, const void* q,
+                const void* k, const void* v, int64_t tok_stride, int64_t head_stride, const float* cos_t,
+                const float* sin_t, void* q_rot, void* out, float* lse, float softmax_scale, void* workspace,
+                size_t workspace_bytes, void* hip_stream) {
+  if (!c) return fail(UNSTEP_E_NULL, "unstep_step: cache handle is NULL");
+  if (!q) return fail(UNSTEP_E_NULL, "unstep_step: q is NULL");
+  AppendPlan p;
+  int rc = plan_append(c, c->idx, start_frame, n_frames, q, k, v, tok_stride, head_stride, cos_t, sin_t, q_rot, &p,
+                       "unstep_step");
+  if (rc != UNSTEP_OK) return rc;
+  unstep::CacheIndex after = c->idx;      // the attention half is checked on the post-append state
+  after.commit_append(start_frame, n_frames);
+  unstep::AttnArgs a;
+  rc = plan_attn(c, after, start_frame, n_frames, window_frames, q_rot, out, lse, softmax_scale, workspace,
+                 workspace_bytes, &a, "unstep_step");
+  if (rc != UNSTEP_OK) return rc;
+  hipStream_t st = static_cast<hipStream_t>(hip_stream);
+  hipError_t e = unstep::launch_rope_append(p.args, st);
+  if (e != hipSuccess) return fail(UNSTEP_E_HIP, "unstep_step (append): %s", hipGetErrorString(e));
+  c->idx = after;
+  e = unstep::launch_window_attn(a, st);
+  if (e != hipSuccess) return fail(UNSTEP_E_HIP, "unstep_step (attention): %s", hipGetErrorString(e));
+  return ok();
+}
+
+}  // extern "C"

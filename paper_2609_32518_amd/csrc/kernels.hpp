@@ -1,0 +1,58 @@
+// Launch descriptors of the step's HIP kernels (gfx950).  Filled and validated by the
+// C ABI layer; the launchers only compute the grid and enqueue.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+#include "unstep.h"
+
+namespace unstep {
+
+constexpr int kHeadDim = UNSTEP_HEAD_DIM;
+
+// Fused rotary embedding of q and k plus the K/V cache write of one chunk.
+struct RopeAppendArgs {
+  const uint16_t* q;       // bf16 [B, N, H, 128] at (tok_stride, head_stride); may be null
+  const uint16_t* k;
+  const uint16_t* v;
+  int64_t tok_stride;      // elements between consecutive tokens
+  int64_t head_stride;     // elements between consecutive heads
+  const float* cos_t;      // [N, 64]
+  const float* sin_t;
+  uint16_t* q_rot;         // bf16 [B, N, H, 128] contiguous; null iff q is null
+  uint16_t* k_cache;       // bf16 [B, H, slots, 128]
+  uint16_t* v_cache;
+  int32_t B, H, T, C;      // batch, heads, tokens per frame, chunk frames
+  int32_t slots;           // cache rows per (batch, head)
+  int32_t f0, S, R;        // start frame, sink frames, ring frames
+};
+
+hipError_t launch_rope_append(const RopeAppendArgs& a, hipStream_t stream);
+
+// Attention of a chunk's queries over the retained cache rows.
+struct AttnArgs {
+  const uint16_t* q;       // bf16 [B, N, H, 128] contiguous (rotated queries)
+  const uint16_t* k_cache; // bf16 [B, H, slots, 128]
+  const uint16_t* v_cache;
+  uint16_t* out;           // bf16 [B, N, H, 128]
+  float* lse;              // [B, H, N] or null
+  float* part_o;           // split-key partial outputs [splits, B, H, N, 128] fp32 (or null)
+  float* part_ml;          // split-key partial (max, sum) [splits, B, H, N, 2] fp32 (or null)
+  int32_t B, N, H, slots;
+  int32_t n_keys;          // retained keys
+  int32_t n_seg;           // key segments (logical order)
+  int32_t seg_l0[UNSTEP_MAX_SEGMENTS + 1];   // logical start of each segment; [n_seg] = n_keys
+  int32_t seg_row0[UNSTEP_MAX_SEGMENTS];     // physical row of each segment's first key
+  int32_t splits;          // key-range splits (1 = none)
+  float scale;             // softmax scale
+};
+
+// Bytes of split-key scratch for `splits` splits (0 when splits <= 1).
+size_t attn_workspace_bytes(int32_t B, int32_t H, int32_t N, int32_t splits);
+// Number of key splits the launcher chooses for this shape.
+int32_t attn_choose_splits(int32_t B, int32_t H, int32_t N, int32_t n_keys);
+hipError_t launch_window_attn(const AttnArgs& a, hipStream_t stream);
+
+}  // namespace unstep

@@ -1,0 +1,93 @@
+// Fused rotary embedding of the chunk's queries and keys plus the K/V cache write
+// (paper Section 3.1 and Appendix A.6): one bandwidth-bound pass over q, k, v.
+//
+// Each thread owns 16 bytes (8 bf16 = 4 coordinate pairs) of one (token, head) row of
+// q, k and v.  It loads them with the token's cos/sin for those 4 pairs, rotates q and
+// k in fp32 and writes q_rot, the rotated key and the value into the cache row of its
+// token: the chunk frame's slot (sink slot f, or ring slot S + (f - S) mod R) times T
+// plus the token's index in the frame.  Consecutive threads cover consecutive 16-byte
+// pieces of a row, then consecutive heads, then consecutive tokens, so the q/k/v reads
+// and the q_rot writes stream contiguously and each cache row is written whole.
+//
+// Rounding: each product and the sum/difference is a separate binary32 operation
+// rounded to nearest-even (floating-point contraction is disabled in this function),
+// and the result is rounded to bf16 nearest-even by v_cvt_pk_bf16_f32.
+#include <hip/hip_runtime.h>
+
+#include "kernels.hpp"
+
+namespace unstep {
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kPieces = kHeadDim / 8;   // 16-byte pieces per head row
+
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ uint32_t rotate_pair(uint32_t w, float c, float s) {
+#pragma clang fp contract(off)
+  const float xe = __uint_as_float(w << 16);
+  const float xo = __uint_as_float(w & 0xffff0000u);
+  const float a = xe * c;
+  const float b = xo * s;
+  const float d = xe * s;
+  const float e = xo * c;
+  const float ye = a - b;
+  const float yo = d + e;
+  bf16x2_t r;
+  r[0] = (__bf16)ye;
+  r[1] = (__bf16)yo;
+  return __builtin_bit_cast(uint32_t, r);
+}
+
+__device__ __forceinline__ uint4 rotate8(uint4 x, float4 c, float4 s) {
+  uint4 y;
+  y.x = rotate_pair(x.x, c.x, s.x);
+  y.y = rotate_pair(x.y, c.y, s.y);
+  y.z = rotate_pair(x.z, c.z, s.z);
+  y.w = rotate_pair(x.w, c.w, s.w);
+  return y;
+}
+
+__global__ __launch_bounds__(kThreads) void rope_append_kernel(RopeAppendArgs a) {
+  const int32_t units = a.T * a.H * kPieces;           // per (batch, frame)
+  const int32_t u = blockIdx.x * kThreads + threadIdx.x;
+  if (u >= units) return;
+  const int32_t piece = u % kPieces;
+  const int32_t r = u / kPieces;
+  const int32_t h = r % a.H;
+  const int32_t t = r / a.H;
+  const int32_t fi = blockIdx.y;                         // frame within the chunk
+  const int32_t b = blockIdx.z;
+  const int32_t f = a.f0 + fi;
+  const int32_t slot = f < a.S ? f : a.S + (f - a.S) % a.R;
+  const int64_t n = int64_t(fi) * a.T + t;
+  const int64_t N = int64_t(a.C) * a.T;
+
+  const int64_t src = (int64_t(b) * N + n) * a.tok_stride + int64_t(h) * a.head_stride + piece * 8;
+  const uint4 kx = *reinterpret_cast<const uint4*>(a.k + src);
+  const uint4 vx = *reinterpret_cast<const uint4*>(a.v + src);
+  const float4 cs = *reinterpret_cast<const float4*>(a.cos_t + n * (kHeadDim / 2) + piece * 4);
+  const float4 sn = *reinterpret_cast<const float4*>(a.sin_t + n * (kHeadDim / 2) + piece * 4);
+  uint4 qx;
+  if (a.q) qx = *reinterpret_cast<const uint4*>(a.q + src);
+
+  const int64_t dst = ((int64_t(b) * a.H + h) * a.slots + int64_t(slot) * a.T + t) * kHeadDim + piece * 8;
+  *reinterpret_cast<uint4*>(a.k_cache + dst) = rotate8(kx, cs, sn);
+  *reinterpret_cast<uint4*>(a.v_cache + dst) = vx;
+  if (a.q) {
+    const int64_t qd = ((int64_t(b) * N + n) * a.H + h) * kHeadDim + piece * 8;
+    *reinterpret_cast<uint4*>(a.q_rot + qd) = rotate8(qx, cs, sn);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_rope_append(const RopeAppendArgs& a, hipStream_t stream) {
+  const int64_t units = int64_t(a.T) * a.H * kPieces;
+  dim3 grid(unsigned((units + kThreads - 1) / kThreads), unsigned(a.C), unsigned(a.B));
+  hipLaunchKernelGGL(rope_append_kernel, grid, dim3(kThreads), 0, stream, a);
+  return hipGetLastError();
+}
+
+}  // namespace unstep

@@ -1,0 +1,195 @@
+"""The C ABI library on the host, without a GPU: it loads, exports every symbol the
+header declares, builds rotary tables bit-identical to the oracle's, keeps the same
+host index state as the oracle's cache model, and rejects bad calls before touching
+the device.  No kernel runs here.
+"""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+import torch
+
+import synth
+from oracle import tables
+from oracle.kvcache import KVCacheOracle, OracleError
+
+u = pytest.importorskip("paper_2609_32518_amd")
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+KIND = {"shape": u.E_SHAPE, "range": u.E_RANGE, "state": u.E_STATE, "null": u.E_NULL}
+
+# fake, 16-byte aligned "device" addresses: host-only calls never dereference them
+FAKE = [0x10000 * (i + 1) for i in range(12)]
+
+
+def header_functions():
+    text = open(os.path.join(ROOT, "include", "unstep.h")).read()
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\*?\s+\*?(unstep_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_every_declared_symbol_is_exported():
+    names = header_functions()
+    assert len(names) >= 13
+    for n in names:
+        assert hasattr(u.lib, n), n
+    assert set(names) == set(u.SIGNATURES)
+
+
+def test_version_and_error_string():
+    assert u.version() == 100
+    assert isinstance(u.lib.unstep_last_error(), bytes)
+
+
+@pytest.mark.parametrize("args", [(9, 3, 30, 52), (6, 3, 4, 6), (0, 1, 1, 1), (59, 1, 30, 52), (123, 3, 5, 7),
+                                  (18, 3, 30, 52)])
+def test_host_tables_bit_identical_to_oracle(args):
+    c, s = u.unstep_rope_tables_host(*args)
+    oc, os_ = tables.rope_tables(*args)
+    assert np.array_equal(c.view(np.uint32), oc.view(np.uint32))
+    assert np.array_equal(s.view(np.uint32), os_.view(np.uint32))
+
+
+def test_tables_argument_errors():
+    buf = np.empty((100, 64), np.float32)
+    p = buf.ctypes.data_as(u._pf32)
+    assert u.lib.unstep_rope_tables_host(0, 1, 2, 2, 64, 10000.0, p, p) == u.E_SHAPE
+    assert u.lib.unstep_rope_tables_host(0, 0, 2, 2, 128, 10000.0, p, p) == u.E_SHAPE
+    assert u.lib.unstep_rope_tables_host(-1, 1, 2, 2, 128, 10000.0, p, p) == u.E_RANGE
+    assert u.lib.unstep_rope_tables_host(0, 1, 2, 2, 128, 1.0, p, p) == u.E_RANGE
+    assert u.lib.unstep_rope_tables_host(0, 1, 2, 2, 128, 10000.0, None, p) == u.E_NULL
+
+
+def _handle(B, H, gh, gw, S, R, head_dim=128, k=FAKE[0], v=FAKE[1]):
+    h = u._vp()
+    rc = u.lib.unstep_cache_create(ctypes.byref(h), B, H, head_dim, gh, gw, S, R, k, v)
+    return rc, h
+
+
+def test_create_errors():
+    assert _handle(1, 2, 2, 3, 0, 4, head_dim=64)[0] == u.E_SHAPE
+    assert _handle(0, 2, 2, 3, 0, 4)[0] == u.E_SHAPE
+    assert _handle(1, 2, 2, 3, -1, 4)[0] == u.E_SHAPE
+    assert _handle(1, 2, 2, 3, 0, 0)[0] == u.E_SHAPE
+    assert _handle(1, 2, 2, 3, 0, 4, k=0)[0] == u.E_NULL
+    assert _handle(1, 2, 2, 3, 0, 4, k=FAKE[0] + 8)[0] == u.E_ALIGN
+    assert u.lib.unstep_cache_destroy(None) == u.OK
+
+
+def _frame_map(h, n):
+    fm = (ctypes.c_int32 * n)()
+    nw = ctypes.c_int32()
+    assert u.lib.unstep_cache_frame_map(h, fm, ctypes.byref(nw)) == u.OK
+    return list(fm), nw.value
+
+
+def _segments(h, f0, C, W):
+    r0 = (ctypes.c_int32 * 4)()
+    ln = (ctypes.c_int32 * 4)()
+    n = ctypes.c_int32()
+    rc = u.lib.unstep_window_segments(h, f0, C, W, r0, ln, ctypes.byref(n))
+    return rc, [(r0[i], ln[i]) for i in range(n.value)] if rc == u.OK else None
+
+
+def _oracle_call(fn):
+    try:
+        return u.OK, fn()
+    except OracleError as e:
+        return KIND[e.kind], None
+
+
+@pytest.mark.parametrize("S,R,C,W", [(0, 9, 3, 6), (3, 6, 3, 3), (0, 12, 1, 11), (2, 4, 1, 2), (1, 5, 2, 3),
+                                     (0, 21, 3, 18), (0, 6, 3, 3)])
+def test_index_state_matches_oracle_over_a_random_call_sequence(S, R, C, W):
+    # random mix of in-order appends, repeated (refine) appends, older re-appends, gaps and
+    # window queries; the library's status, frame map and segments must equal the oracle's
+    gh, gw = 2, 3
+    rc, h = _handle(1, 1, gh, gw, S, R)
+    assert rc == u.OK
+    orc = KVCacheOracle(1, 1, 128, gh, gw, S, R)
+    rng = np.random.default_rng(S * 1000 + R * 100 + C * 10 + W)
+    zeros = np.zeros((1, C * gh * gw, 1, 128), np.uint16)
+    try:
+        for step in range(300):
+            op = rng.integers(0, 4)
+            f0 = int(max(0, orc.newest + 1 + rng.integers(-2 * R, 3)))
+            if op <= 1:
+                code, _ = _oracle_call(lambda: orc.append(f0, C, zeros, zeros))
+                assert u.lib.unstep_cache_advance(h, f0, C) == code, (step, f0)
+            else:
+                w = int(rng.integers(0, W + 3))
+                code, segs = _oracle_call(lambda: orc.segments(f0, C, w))
+                rc, got = _segments(h, f0, C, w)
+                assert rc == code, (step, f0, w)
+                if code == u.OK:
+                    assert got == segs
+                    rows = orc.key_rows(f0, C, w)
+                    assert sum(l for _, l in got) == rows.size
+            fm, newest = _frame_map(h, S + R)
+            assert fm == orc.frame_of_slot and newest == orc.newest
+    finally:
+        u.lib.unstep_cache_destroy(h)
+
+
+def test_paper_window_segments_and_key_counts():
+    # 3 sinks + 6 recent frames including the chunk (14040 keys at 30x52), ring of 6
+    rc, h = _handle(1, 12, 30, 52, 3, 6)
+    for f0 in range(0, 12, 3):
+        assert u.lib.unstep_cache_advance(h, f0, 3) == u.OK
+    rc, segs = _segments(h, 9, 3, 3)
+    assert rc == u.OK and sum(l for _, l in segs) == 14040
+    assert segs == [(0, 3 * 1560), (6 * 1560, 3 * 1560), (3 * 1560, 3 * 1560)]
+    u.lib.unstep_cache_destroy(h)
+
+
+def test_append_errors_are_caught_before_any_device_work():
+    rc, h = _handle(1, 2, 2, 3, 0, 4)
+    T = 6
+    p = FAKE
+    args = lambda f0, C, q=None, qr=None, ts=256, hs=128, k=p[2]: (h, f0, C, q, k, p[3], ts, hs, p[4], p[5], qr, None)
+    assert u.lib.unstep_kv_append(*args(1, 1)) == u.E_STATE              # gap
+    assert u.lib.unstep_kv_append(*args(0, 0)) == u.E_SHAPE              # empty chunk
+    assert u.lib.unstep_kv_append(*args(-1, 1)) == u.E_RANGE
+    assert u.lib.unstep_kv_append(*args(0, 5)) == u.E_RANGE              # more than the ring
+    assert u.lib.unstep_kv_append(*args(0, 1, k=None)) == u.E_NULL
+    assert u.lib.unstep_kv_append(*args(0, 1, q=p[6])) == u.E_NULL       # q without q_rot
+    assert u.lib.unstep_kv_append(*args(0, 1, ts=200)) == u.E_SHAPE      # tokens overlap
+    assert u.lib.unstep_kv_append(*args(0, 1, ts=264, hs=132)) == u.E_ALIGN
+    assert u.lib.unstep_kv_append(*args(0, 1, k=p[2] + 4)) == u.E_ALIGN
+    assert u.lib.unstep_kv_append(None, 0, 1, None, p[2], p[3], 256, 128, p[4], p[5], None, None) == u.E_NULL
+    assert _frame_map(h, 4) == ([-1] * 4, -1)
+    # attention: nothing stored yet
+    out = (h, 0, 1, 0, p[6], p[7], None, 0.0, None, 0, None)
+    assert u.lib.unstep_window_attn(*out) == u.E_STATE
+    assert u.lib.unstep_window_attn(h, 0, 1, 0, None, p[7], None, 0.0, None, 0, None) == u.E_NULL
+    assert u.lib.unstep_cache_advance(h, 0, 3) == u.OK
+    assert u.lib.unstep_window_attn(h, 3, 1, 3, p[6], p[7], None, 0.0, None, 0, None) == u.E_STATE
+    assert u.lib.unstep_window_attn(h, 3, 2, 3, p[6], p[7], None, 0.0, None, 0, None) == u.E_RANGE  # 5 > 4 ring frames
+    assert u.lib.unstep_window_attn(h, 2, 1, 2, p[6] + 2, p[7], None, 0.0, None, 0, None) == u.E_ALIGN
+    # step: the attention half is checked on the post-append state, before anything runs
+    st = lambda f0, C, W: u.lib.unstep_step(h, f0, C, W, p[6], p[2], p[3], 256, 128, p[4], p[5], p[8], p[9],
+                                            None, 0.0, None, 0, None)
+    assert st(3, 2, 3) == u.E_RANGE                                     # 3 prior + 2 > 4 ring frames
+    assert st(5, 1, 1) == u.E_STATE                                     # gap
+    assert _frame_map(h, 4) == ([0, 1, 2, -1], 2)
+    u.lib.unstep_cache_destroy(h)
+
+
+@pytest.mark.skipif(torch.cuda.is_available(), reason="checks the no-device error path")
+def test_launch_failure_leaves_state_unchanged_without_a_device():
+    rc, h = _handle(1, 2, 2, 3, 0, 4)
+    p = FAKE
+    rc = u.lib.unstep_kv_append(h, 0, 1, None, p[2], p[3], 256, 128, p[4], p[5], None, None)
+    assert rc == u.E_HIP and u.lib.unstep_last_error()
+    assert _frame_map(h, 4) == ([-1] * 4, -1)
+    u.lib.unstep_cache_destroy(h)
+
+
+def test_workspace_size_is_shape_only():
+    rc, h = _handle(1, 12, 30, 52, 0, 12)
+    b = ctypes.c_size_t()
+    # nothing stored: the size query still answers (it depends on shapes only)
+    assert u.lib.unstep_attn_workspace_size(h, 0, 1, 11, ctypes.byref(b)) == u.OK
+    assert u.lib.unstep_attn_workspace_size(h, 0, 0, 11, ctypes.byref(b)) == u.E_SHAPE
+    u.lib.unstep_cache_destroy(h)
