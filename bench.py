@@ -1,0 +1,262 @@
+"""Benchmark of the windowed-attention chunk step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload full_chunk]
+                    [--sets 4] [--no-cpu-baseline]
+
+A step is one whole pass of the hot path over one chunk: the fused RoPE + KV append
+and the windowed attention (unstep_step).  The default workload is the full-frame
+chunk: 12 heads of width 128, a 30x52 token grid, a 3-frame chunk (4680 queries) at
+latent frame 9 over 9 prior frames (18720 retained keys).  Other workloads:
+unwindowed (32760 keys), paper_default (3 sinks + 6 recent frames, 14040 keys),
+short_refine (one step = 30 layers x 2 calls over 9360 keys) and rolling (one step =
+60 one-frame chunks through a 12-frame ring from empty).
+
+Inputs are synthetic, seeded N(0,1) bf16, resident in HBM before timing.  Several
+buffer sets (cache + inputs + outputs) are rotated so that consecutive steps do not
+find their data in the 256 MB Infinity Cache.  W warm-up steps, then K timed steps
+between device synchronisations; per-kernel durations come from HIP events recorded
+on the stream the kernels run on, in a second loop over the same work.
+
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import platform
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "windowed-attn TFLOP/s + µs per chunk-step (12×128 heads, 4680 q); RoPE GB/s"
+PEAK_BF16_TFLOPS = 2500.0     # MI355X dense bf16 MFMA, published
+PEAK_HBM_GBS = 8000.0         # MI355X HBM3E, published
+
+
+def parse():
+    p = argparse.ArgumentParser()
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=50)
+    p.add_argument("--warmup", type=int, default=10)
+    p.add_argument("--workload", default="full_chunk")
+    p.add_argument("--sets", type=int, default=4)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-queries", type=int, default=2048, help="oracle sample: queries x all heads")
+    return p.parse_args()
+
+
+def attn_flops(H, Nq, Nk, D=128):
+    return 4.0 * H * Nq * Nk * D
+
+
+def rope_bytes(H, Nq, D=128):
+    # read q, k, v + write q_rot, K row, V row (bf16) + cos, sin (fp32, D/2 each) per token
+    return Nq * (12 * H * D + 4 * D)
+
+
+class Plan:
+    """The step's work for one workload: a list of (cache set, start frame, frames, window)."""
+
+    def __init__(self, u, torch, wl, n_sets):
+        self.u, self.torch, self.wl = u, torch, wl
+        dev = "cuda"
+        g = torch.Generator(device=dev)
+        N = wl.n_query
+
+        def randn(shape, seed):
+            g.manual_seed(seed)
+            return torch.randn(shape, generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+
+        self.tables = u.RopeTableCache(dev)
+        self.sets = []
+        if wl.name == "short_refine":
+            n_caches = wl.layers                      # one cache per layer; the layers rotate HBM
+        elif wl.name == "rolling":
+            n_caches = n_sets
+        else:
+            n_caches = n_sets
+        for si in range(n_caches):
+            cache = u.Cache(wl.B, wl.H, wl.grid_h, wl.grid_w, wl.S, wl.R, device=dev)
+            shape = (wl.B, N, wl.H, 128)
+            s = dict(cache=cache, q=randn(shape, 10 * si + 1), k=randn(shape, 10 * si + 2),
+                     v=randn(shape, 10 * si + 3), q_rot=torch.empty(shape, dtype=torch.bfloat16, device=dev),
+                     out=torch.empty(shape, dtype=torch.bfloat16, device=dev))
+            if wl.name != "rolling":
+                self._prefill(cache, randn, 1000 * (si + 1))
+            self.sets.append(s)
+        # per step: list of (set index, start frame, frames, window)
+        if wl.name == "short_refine":
+            self.calls = [(layer, wl.f0, wl.C, wl.W) for layer in range(wl.layers) for _ in range(wl.passes)]
+        elif wl.name == "rolling":
+            self.calls = [(None, c, 1, wl.W) for c in range(wl.chunks)]
+        else:
+            self.calls = [(None, wl.f0, wl.C, wl.W)]
+        for (_, f0, C, W) in self.calls:
+            self.tables.get(f0, C, wl.grid_h, wl.grid_w)
+        self.ws = {}
+        for si, s in enumerate(self.sets):
+            for (_, f0, C, W) in self.calls:
+                need = s["cache"].workspace_bytes(f0, C, W)
+                if need and need > self.ws.get(si, torch.empty(0)).numel():
+                    self.ws[si] = torch.empty(need, dtype=torch.uint8, device=dev)
+        self.step_idx = 0
+
+    def _prefill(self, cache, randn, seed):
+        wl = self.wl
+        for f0 in range(0, wl.f0, wl.C):
+            shape = (wl.B, wl.C * wl.T, wl.H, 128)
+            cos_t, sin_t = self.tables.get(f0, wl.C, wl.grid_h, wl.grid_w)
+            cache.unstep_kv_append(f0, wl.C, None, randn(shape, seed + f0), randn(shape, seed + f0 + 500), cos_t,
+                                   sin_t)
+
+    def keys(self, f0, C, W):
+        wl = self.wl
+        lo = max(0, f0 - W)
+        return (min(wl.S, lo) + f0 + C - lo) * wl.T
+
+    def per_step(self):
+        wl = self.wl
+        fl = sum(attn_flops(wl.H, C * wl.T, self.keys(f0, C, W)) * wl.B for (_, f0, C, W) in self.calls)
+        by = sum(rope_bytes(wl.H, C * wl.T) * wl.B for (_, f0, C, W) in self.calls)
+        return fl, by
+
+    def _set_for(self, call_set):
+        if call_set is not None:
+            return call_set
+        return self.step_idx % len(self.sets)
+
+    def step(self, events=None):
+        """Enqueue one step.  With `events` (list), record (append_start, append_end=attn_start,
+        attn_end) events around each call's two kernels."""
+        torch, wl = self.torch, self.wl
+        if wl.name == "rolling":
+            si = self.step_idx % len(self.sets)
+            s = self.sets[si]
+            s["cache"] = self.u.Cache(wl.B, wl.H, wl.grid_h, wl.grid_w, wl.S, wl.R, k_cache=s["cache"].k,
+                                      v_cache=s["cache"].v)
+        for (cs, f0, C, W) in self.calls:
+            si = self._set_for(cs)
+            s = self.sets[si]
+            N = C * wl.T
+            cos_t, sin_t = self.tables.get(f0, C, wl.grid_h, wl.grid_w)
+            q, k, v = s["q"][:, :N], s["k"][:, :N], s["v"][:, :N]
+            q_rot, out = s["q_rot"][:, :N], s["out"][:, :N]
+            ws = self.ws.get(si)
+            if events is None:
+                s["cache"].unstep_step(f0, C, W, q, k, v, cos_t, sin_t, q_rot=q_rot, out=out, workspace=ws)
+            else:
+                e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
+                e0.record()
+                s["cache"].unstep_kv_append(f0, C, q, k, v, cos_t, sin_t, q_rot=q_rot)
+                e1.record()
+                s["cache"].unstep_window_attn(f0, C, W, q_rot, out=out, workspace=ws)
+                e2.record()
+                events.append((e0, e1, e2, C * wl.T, self.keys(f0, C, W)))
+        self.step_idx += 1
+
+
+def cpu_baseline(wl, n_queries):
+    """The oracle, untuned, on a bounded sample of the workload: RoPE of one chunk's q and k,
+    then exact attention of n_queries queries (all heads) over the retained keys."""
+    import numpy as np
+
+    import synth
+    from oracle import attention, rope, tables
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = len(os.sched_getaffinity(0))
+    N = wl.n_query
+    shape = (wl.B, N, wl.H, 128)
+    q = synth.normal_bf16(shape, (90, synth.Q))
+    k = synth.normal_bf16(shape, (90, synth.K))
+    nk = (min(wl.S, max(0, wl.f0 - wl.W)) + wl.f0 + wl.C - max(0, wl.f0 - wl.W)) * wl.T
+    kc = synth.normal_bf16((wl.B, wl.H, nk, 128), (90, synth.CACHE_K))
+    vc = synth.normal_bf16((wl.B, wl.H, nk, 128), (90, synth.CACHE_V))
+    nq = min(n_queries, N)
+    t0 = time.perf_counter()
+    c, s = tables.rope_tables(wl.f0, wl.C, wl.grid_h, wl.grid_w)
+    qr = rope.rope_bf16(q, c, s)
+    rope.rope_bf16(k, c, s)
+    attention.attention(qr, kc, vc, np.arange(nk), query_idx=np.arange(nq))
+    dt = time.perf_counter() - t0
+    flops = attn_flops(wl.H, nq, nk) * wl.B
+    return {"value": round(flops / dt / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"fp64 NumPy oracle: rotary tables + RoPE of one {N}-token chunk's q and k, then attention "
+                      f"of {nq} of its {N} queries x {wl.H} heads over {nk} keys; {dt:.2f} s wall; "
+                      f"{len(os.sched_getaffinity(0))} host cores visible, {platform.processor() or 'cpu'}"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py: this build measures one GPU only (the step shards by head across GPUs, but no "
+              f"multi-GPU path is built); got --gpus {args.gpus}", file=sys.stderr)
+        sys.exit(2)
+    import torch
+
+    import synth
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    import paper_2609_32518_amd as u
+
+    wl = synth.WORKLOADS[args.workload]
+    plan = Plan(u, torch, wl, args.sets)
+    flops, rbytes = plan.per_step()
+    torch.cuda.synchronize()
+
+    for _ in range(args.warmup):
+        plan.step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        plan.step()
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    ms = dt * 1e3 / args.steps
+
+    # per-kernel durations: HIP events on the launch stream around each kernel
+    events = []
+    for _ in range(args.steps):
+        plan.step(events)
+    torch.cuda.synchronize()
+    t_app = [e0.elapsed_time(e1) * 1e3 for (e0, e1, e2, nq, nk) in events]     # us
+    t_att = [e1.elapsed_time(e2) * 1e3 for (e0, e1, e2, nq, nk) in events]
+    fl_att = [attn_flops(wl.H, nq, nk) * wl.B for (e0, e1, e2, nq, nk) in events]
+    by_app = [rope_bytes(wl.H, nq) * wl.B for (e0, e1, e2, nq, nk) in events]
+    attn_us = sum(t_att) / len(t_att)
+    app_us = sum(t_app) / len(t_app)
+    attn_tflops = sum(fl_att) / (sum(t_att) * 1e-6) / 1e12
+    rope_gbs = sum(by_app) / (sum(t_app) * 1e-6) / 1e9
+
+    value = flops / (ms * 1e-3) / 1e12
+    res = {
+        "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.name, "batch": wl.B, "heads": wl.H, "head_dim": 128,
+                   "grid": [wl.grid_h, wl.grid_w], "chunk_frames": wl.C, "sink_frames": wl.S,
+                   "window_frames": wl.W, "ring_frames": wl.R, "queries": wl.n_query,
+                   "keys": plan.keys(wl.f0, wl.C, wl.W), "calls_per_step": len(plan.calls),
+                   "buffer_sets": len(plan.sets), "parallelism": "single GPU"},
+        "us_per_step": round(ms * 1e3, 2),
+        "attn": {"kernel": "window_attn", "us_per_call": round(attn_us, 2), "tflops": round(attn_tflops, 2)},
+        "rope_append": {"kernel": "rope_append", "us_per_call": round(app_us, 2), "gbs": round(rope_gbs, 1)},
+        "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 2), "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None},
+        "rope_roofline": {"bound": "hbm", "achieved": round(rope_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                          "frac": round(rope_gbs / PEAK_HBM_GBS, 4), "traffic": None},
+    }
+    if not args.no_cpu_baseline:
+        res["cpu_baseline"] = cpu_baseline(wl, args.cpu_queries)
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

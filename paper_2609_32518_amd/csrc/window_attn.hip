@@ -267,12 +267,30 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
 }  // namespace
 
 int32_t attn_choose_splits(int32_t B, int32_t H, int32_t N, int32_t n_keys) {
+  // Estimated time of s splits: rounds of resident work-groups (256 compute units x 2)
+  // times the key tiles each work-group walks, plus the combine's traffic (partials
+  // written and read back, fp32) at a sustained 5 TB/s.  A split keeps >= 4 tiles.
+  constexpr int64_t kSlots = 256 * 2;
+  constexpr double kTileUs = 2.0;             // one 128-query x 64-key tile per work-group
+  constexpr double kBytesPerUs = 5.0e6;
   const int64_t groups = int64_t(B) * H * ((N + kBlockQ - 1) / kBlockQ);
   const int32_t tiles = (n_keys + kBlockK - 1) / kBlockK;
-  // aim for at least two work-groups per compute unit (256 CUs), keep >= 8 tiles per split
-  int32_t splits = 1;
-  while (groups * splits < 512 && tiles / (splits * 2) >= 8 && splits < 16) splits *= 2;
-  return splits;
+  auto cost = [&](int32_t s) {
+    const int64_t rounds = (groups * s + kSlots - 1) / kSlots;
+    const double walk = double(rounds) * double((tiles + s - 1) / s) * kTileUs;
+    const double comb = s > 1 ? double(s) * B * H * N * (kHeadDim + 2) * 4.0 * 2.0 / kBytesPerUs : 0.0;
+    return walk + comb;
+  };
+  int32_t best = 1;
+  double best_cost = cost(1);
+  for (int32_t s = 2; s <= 8 && tiles / s >= 4; ++s) {
+    const double c = cost(s);
+    if (c < best_cost) {
+      best = s;
+      best_cost = c;
+    }
+  }
+  return best;
 }
 
 size_t attn_workspace_bytes(int32_t B, int32_t H, int32_t N, int32_t splits) {

@@ -34,8 +34,9 @@ def bf16_bits_from_f32(x: np.ndarray) -> np.ndarray:
 
     Used only to turn random draws into bf16 inputs; NaN never occurs here.
     """
-    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32).astype(np.uint64)
-    u = (u + 0x7FFF + ((u >> 16) & 1)) >> 16
+    u = np.ascontiguousarray(x, dtype=np.float32).view(np.uint32)
+    # finite values stay below 2^32 - 0x8000 after the increment, so 32 bits suffice
+    u = (u + np.uint32(0x7FFF) + ((u >> np.uint32(16)) & np.uint32(1))) >> np.uint32(16)
     return u.astype(np.uint16)
 
 
