@@ -4,17 +4,27 @@
 // UNSTEP_MAX_SEGMENTS runs of consecutive cache rows, so a ring that wraps is read in
 // place: the tile loader maps each logical key index to its physical row.
 //
-// Work-group: 4 waves x 32 queries = 128 queries of one (batch, head), optionally one
-// of `splits` contiguous key ranges.  Per 64-key tile:
-//   S^T = K_tile * Q^T   (v_mfma_f32_32x32x16_bf16; keys on the M side, queries on N),
-// so each lane owns one query column and 32 of the tile's keys (the partner lane
-// l^32 owns the other 32): row max and row sum are in-lane plus one exchange.
-//   O^T += V^T * P^T     (same MFMA; P^T comes straight from the S^T registers)
-// The MFMA contracts over 16 "k" slots per lane pair; the keys behind those slots are
-// permuted to match where the S^T accumulator left them, and V^T is read from LDS with
-// the same permutation.  Softmax runs in fp32 with base-2 exponentials of
-// (s - max) * scale * log2(e); the running output is rescaled when the max grows.
+// Work-group: 4 waves x 32 queries (kQB = 1; two work-groups per compute unit, so two
+// waves per SIMD from independent work-groups overlap one's MFMAs with the other's
+// softmax), optionally one of `splits` contiguous key ranges.  Per 64-key tile, per wave:
+//   S^T = K_tile * Q^T   (v_mfma_f32_32x32x16_bf16, keys on the M side, queries on N):
+//       each lane owns one query column and 32 of the tile's keys, the partner lane
+//       l^32 the other 32, so row max and row sum are in-lane plus one exchange.
+//   O^T += V^T * P^T     (same MFMA): P^T comes straight from the S^T registers; the
+//       MFMA's 16 contraction slots per lane pair are mapped to the keys where the S^T
+//       accumulator left them, and the matching V^T fragments are read from the
+//       row-major V tile with the transposing LDS read ds_read_b64_tr_b16.
+// K and V tiles are double-buffered in LDS; the next tile's global loads are issued
+// before the current tile's MFMAs and written to the other buffer after them (one
+// barrier per tile).
+// Softmax: fp32, base-2 exponentials of (s - m) * scale * log2(e) with a fixed per-row
+// offset m (the max of the range's first tile), so the loop never rescales the output;
+// if a row's sum exceeds 2^64 the work-group redoes its range with the exact row max
+// (see window_attn_kernel).  Row sums accumulate the bf16-rounded probabilities that
+// enter the PV product (v_dot2_f32_bf16).
 //
+// Work-groups are numbered so that consecutive logical units (same head, neighbouring
+// query tiles) land on the same XCD and share its L2 while they stream the same keys.
 // With splits > 1 each work-group writes its normalised partial output and its
 // (max, sum) to the workspace and attn_combine merges them by log-sum-exp.
 #include <hip/hip_runtime.h>
@@ -28,32 +38,246 @@ namespace {
 
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
-constexpr int kQPerWave = 32;
-constexpr int kBlockQ = kWaves * kQPerWave;   // 128 queries per work-group
 constexpr int kBlockK = 64;                   // keys per tile
-constexpr int kKStride = kHeadDim + 8;        // LDS row of K (bf16), padded
-constexpr int kVStride = kBlockK + 4;         // LDS row of V^T (bf16), padded
+#ifndef UNSTEP_ATTN_QB
+#define UNSTEP_ATTN_QB 1
+#endif
+// 32-query blocks per wave: 1 -> 128 queries per work-group and two work-groups per
+// compute unit (two waves per SIMD); 2 -> 256 queries per work-group, one wave per SIMD.
+constexpr int kQB = UNSTEP_ATTN_QB;
+constexpr int kQPerWave = 32 * kQB;
+constexpr int kBlockQ = kWaves * kQPerWave;
+constexpr int kGroupsPerCU = kQB == 1 ? 2 : 1;
+// LDS row strides (bf16 elements).  K: 68 dwords, so the 16 lanes of each b128 read
+// phase (16 rows, same columns) cover all 64 banks once.  V: 80 dwords, so each half-wave
+// of a transposing b64 read (4 rows x 64 bytes) covers all 64 banks once.
+constexpr int kKStride = kHeadDim + 8;
+constexpr int kVStride = kHeadDim + 32;
 constexpr float kLog2e = 1.4426950408889634f;
+constexpr int kXcds = 8;
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
 
 struct Smem {
-  uint16_t k[kBlockK * kKStride];
-  uint16_t vt[kHeadDim * kVStride];
+  uint16_t k[2][kBlockK * kKStride];
+  uint16_t v[2][kBlockK * kVStride];
 };
 
-__device__ __forceinline__ int32_t key_row(const AttnArgs& a, int32_t key) {
-  int32_t l0 = a.seg_l0[0], r0 = a.seg_row0[0];
-#pragma unroll
-  for (int s = 1; s < UNSTEP_MAX_SEGMENTS; ++s)
-    if (key >= a.seg_l0[s]) { l0 = a.seg_l0[s]; r0 = a.seg_row0[s]; }
-  return r0 + (key - l0);
+// Physical cache row of a logical key index: up to four runs of consecutive rows, the
+// first starting at logical index 0.  Held in scalar registers, resolved with selects.
+struct SegTable {
+  int32_t l1, l2, l3;          // logical start of runs 1..3 (INT32_MAX when absent)
+  int32_t r0, r1, r2, r3;      // physical row of each run's first key
+  __device__ __forceinline__ int32_t row(int32_t key) const {
+    int32_t r = r0 + key;
+    r = key >= l1 ? r1 + (key - l1) : r;
+    r = key >= l2 ? r2 + (key - l2) : r;
+    r = key >= l3 ? r3 + (key - l3) : r;
+    return r;
+  }
+};
+
+__device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t u) { return __builtin_bit_cast(bf16x8_t, u); }
+
+// Transposing LDS read: within each 16-lane group, lane i receives element (i & 3) of
+// the 4 x b16 rows addressed by lanes 4e + (i >> 2), e = 0..3.
+__device__ __forceinline__ u32x2_t lds_read_tr(const uint16_t* p) {
+  const i16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(p));
+  return __builtin_bit_cast(u32x2_t, v);
 }
 
-__device__ __forceinline__ bf16x8_t as_bf16x8(uint4 u) { return __builtin_bit_cast(bf16x8_t, u); }
+// Everything one work-group needs while it walks its key range.
+struct Walk {
+  const uint16_t* kbase;       // this (batch, head)'s K rows
+  const uint16_t* vbase;
+  SegTable seg;
+  int32_t k_begin, k_end;      // logical key range
+  int tid, col, half, vsrc;
+  float c2;                    // scale * log2(e)
+};
 
-__global__ __launch_bounds__(kThreads, 2) void window_attn_kernel(AttnArgs a) {
+// One 64-key tile's 16-byte pieces for this thread: (row, piece) = (c >> 4, c & 15),
+// c = tid + 256 j.  Keys past the range read the range's last key (finite values whose
+// scores are masked to -inf).
+struct TileRegs {
+  u32x4_t k0, k1, k2, k3;
+  u32x4_t v0, v1, v2, v3;
+};
+
+__device__ __forceinline__ void load_piece(u32x4_t& kx, u32x4_t& vx, const Walk& w, int32_t kt0, int j) {
+  const int c = w.tid + kThreads * j;
+  const int32_t key = min(kt0 + (c >> 4), w.k_end - 1);
+  const int64_t off = int64_t(w.seg.row(key)) * kHeadDim + (c & 15) * 8;
+  kx = *reinterpret_cast<const u32x4_t*>(w.kbase + off);
+  vx = *reinterpret_cast<const u32x4_t*>(w.vbase + off);
+}
+
+__device__ __forceinline__ void load_tile(TileRegs& r, const Walk& w, int32_t kt0) {
+  load_piece(r.k0, r.v0, w, kt0, 0);
+  load_piece(r.k1, r.v1, w, kt0, 1);
+  load_piece(r.k2, r.v2, w, kt0, 2);
+  load_piece(r.k3, r.v3, w, kt0, 3);
+}
+
+__device__ __forceinline__ void store_piece(Smem& sm, int buf, const u32x4_t& kx, const u32x4_t& vx, int tid, int j) {
+  const int c = tid + kThreads * j;
+  *reinterpret_cast<u32x4_t*>(&sm.k[buf][(c >> 4) * kKStride + (c & 15) * 8]) = kx;
+  *reinterpret_cast<u32x4_t*>(&sm.v[buf][(c >> 4) * kVStride + (c & 15) * 8]) = vx;
+}
+
+__device__ __forceinline__ void store_tile(Smem& sm, int buf, const TileRegs& r, int tid) {
+  store_piece(sm, buf, r.k0, r.v0, tid, 0);
+  store_piece(sm, buf, r.k1, r.v1, tid, 1);
+  store_piece(sm, buf, r.k2, r.v2, tid, 2);
+  store_piece(sm, buf, r.k3, r.v3, tid, 3);
+}
+
+// S^T for key block kb of the tile in LDS: both 32-query blocks share each K fragment.
+__device__ __forceinline__ void qk_block(f32x16_t (&s)[kQB], const uint16_t* kt, const bf16x8_t (&qf)[kQB][8], int kb,
+                                         const Walk& w) {
+  const f32x16_t zero = {};
+#pragma unroll
+  for (int st = 0; st < 8; ++st) {
+    const bf16x8_t kf =
+        as_bf16x8(*reinterpret_cast<const u32x4_t*>(&kt[(kb * 32 + w.col) * kKStride + 16 * st + 8 * w.half]));
+#pragma unroll
+    for (int qb = 0; qb < kQB; ++qb)
+      s[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][st], st == 0 ? zero : s[qb], 0, 0, 0);
+  }
+}
+
+__device__ __forceinline__ void mask_block(f32x16_t (&s)[kQB], int32_t key0, int32_t k_end, int half) {
+#pragma unroll
+  for (int qb = 0; qb < kQB; ++qb)
+#pragma unroll
+    for (int i = 0; i < 16; ++i)
+      if (key0 + 8 * (i >> 2) + 4 * half + (i & 3) >= k_end) s[qb][i] = -INFINITY;
+}
+
+// Probabilities (bf16) of key block kb and their row sums, then O^T += V^T * P^T over
+// the block's two 16-key steps.
+__device__ __forceinline__ void pv_block(f32x16_t (&o)[kQB][4], float (&l)[kQB], const f32x16_t (&s)[kQB],
+                                         const uint16_t* vt, int kb, const float (&m_off)[kQB], const Walk& w) {
+  const bf16x2_t ones = {(__bf16)1.f, (__bf16)1.f};
+  bf16x8_t pf[kQB][2];
+#pragma unroll
+  for (int qb = 0; qb < kQB; ++qb) {
+    const float moff = m_off[qb] * w.c2;
+    float acc = l[qb];
+#pragma unroll
+    for (int i = 0; i < 16; i += 2) {
+      bf16x2_t p2;
+      p2[0] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s[qb][i], w.c2, -moff));
+      p2[1] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s[qb][i + 1], w.c2, -moff));
+      acc = __builtin_amdgcn_fdot2_f32_bf16(p2, ones, acc, false);
+      pf[qb][i >> 3][i & 7] = p2[0];
+      pf[qb][i >> 3][(i & 7) + 1] = p2[1];
+    }
+    l[qb] = acc;
+  }
+#pragma unroll
+  for (int sub = 0; sub < 2; ++sub) {
+    const int t = kb * 2 + sub;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) {
+      const u32x2_t lo = lds_read_tr(vt + (16 * t) * kVStride + 32 * d);
+      const u32x2_t hi = lds_read_tr(vt + (16 * t + 8) * kVStride + 32 * d);
+      const bf16x8_t vf = as_bf16x8(u32x4_t{lo.x, lo.y, hi.x, hi.y});
+#pragma unroll
+      for (int qb = 0; qb < kQB; ++qb)
+        o[qb][d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[qb][sub], o[qb][d], 0, 0, 0);
+    }
+  }
+}
+
+// Walk the key range once with fixed per-row exponent offsets m_off (raw score units).
+// kFromFirstTile: set m_off from the first tile's row max (pass 0); otherwise m_off is
+// given (the exact row max).  Accumulates O^T (o) and the row sums (l) from zero.
+template <bool kFromFirstTile>
+__device__ __forceinline__ void attend(Smem& sm, const Walk& w, const bf16x8_t (&qf)[kQB][8], float (&m_off)[kQB],
+                                       f32x16_t (&o)[kQB][4], float (&l)[kQB]) {
+  const f32x16_t zero = {};
+#pragma unroll
+  for (int qb = 0; qb < kQB; ++qb) {
+    l[qb] = 0.f;
+#pragma unroll
+    for (int d = 0; d < 4; ++d) o[qb][d] = zero;
+  }
+  TileRegs pre;
+  if (w.k_begin < w.k_end) {
+    load_tile(pre, w, w.k_begin);
+    store_tile(sm, 0, pre, w.tid);
+  }
+  __syncthreads();
+
+  int buf = 0;
+  for (int32_t kt0 = w.k_begin; kt0 < w.k_end; kt0 += kBlockK, buf ^= 1) {
+    const bool has_next = kt0 + kBlockK < w.k_end;
+    if (has_next) load_tile(pre, w, kt0 + kBlockK);
+    const uint16_t* kt = sm.k[buf];
+    const uint16_t* vt = sm.v[buf] + w.vsrc;
+    const bool last = kt0 + kBlockK > w.k_end;
+
+    f32x16_t s0[kQB], s1[kQB];
+    qk_block(s0, kt, qf, 0, w);
+    qk_block(s1, kt, qf, 1, w);
+    if (last) {
+      mask_block(s0, kt0, w.k_end, w.half);
+      mask_block(s1, kt0 + 32, w.k_end, w.half);
+    }
+    if (kFromFirstTile && kt0 == w.k_begin) {
+#pragma unroll
+      for (int qb = 0; qb < kQB; ++qb) {
+        float m = s0[qb][0];
+#pragma unroll
+        for (int i = 0; i < 16; ++i) m = fmaxf(fmaxf(m, s0[qb][i]), s1[qb][i]);
+        m_off[qb] = fmaxf(m, __shfl_xor(m, 32));
+      }
+    }
+
+    pv_block(o, l, s0, vt, 0, m_off, w);
+    pv_block(o, l, s1, vt, 1, m_off, w);
+
+    if (has_next) store_tile(sm, buf ^ 1, pre, w.tid);
+    __syncthreads();
+  }
+}
+
+// Exact row max of the scores over the key range (QK only), for the overflow fallback.
+__device__ __forceinline__ void exact_row_max(Smem& sm, const Walk& w, const bf16x8_t (&qf)[kQB][8],
+                                              float (&m_off)[kQB]) {
+  float mx[kQB];
+#pragma unroll
+  for (int qb = 0; qb < kQB; ++qb) mx[qb] = -INFINITY;
+  TileRegs r;
+  for (int32_t kt0 = w.k_begin; kt0 < w.k_end; kt0 += kBlockK) {
+    __syncthreads();
+    load_tile(r, w, kt0);
+    store_tile(sm, 0, r, w.tid);
+    __syncthreads();
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      f32x16_t s[kQB];
+      qk_block(s, sm.k[0], qf, kb, w);
+      mask_block(s, kt0 + 32 * kb, w.k_end, w.half);
+#pragma unroll
+      for (int qb = 0; qb < kQB; ++qb)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) mx[qb] = fmaxf(mx[qb], s[qb][i]);
+    }
+  }
+#pragma unroll
+  for (int qb = 0; qb < kQB; ++qb) m_off[qb] = fmaxf(mx[qb], __shfl_xor(mx[qb], 32));
+  __syncthreads();
+}
+
+__global__ __launch_bounds__(kThreads, kGroupsPerCU) void window_attn_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) Smem sm;
 
   const int tid = threadIdx.x;
@@ -62,136 +286,83 @@ __global__ __launch_bounds__(kThreads, 2) void window_attn_kernel(AttnArgs a) {
   const int half = lane >> 5;
   const int col = lane & 31;
 
-  const int32_t h = blockIdx.y;
-  const int32_t b = blockIdx.z / a.splits;
-  const int32_t split = blockIdx.z % a.splits;
-  const int32_t qi = blockIdx.x * kBlockQ + wave * kQPerWave + col;
-  const int32_t qc = qi < a.N ? qi : a.N - 1;
+  // XCD-aware numbering: hardware work-group g runs on XCD g % 8; give each XCD a
+  // contiguous range of logical units.
+  const int32_t G = gridDim.x;
+  const int32_t xcd = blockIdx.x % kXcds;
+  const int32_t unit = xcd * (G / kXcds) + min(xcd, G % kXcds) + blockIdx.x / kXcds;
+  const int32_t N = a.N, H = a.H;
+  const int32_t qtiles = (N + kBlockQ - 1) / kBlockQ;
+  const int32_t qt = unit % qtiles;
+  const int32_t rest = unit / qtiles;
+  const int32_t split = rest % a.splits;
+  const int32_t bh_idx = rest / a.splits;          // b * H + h
+  const int32_t h = bh_idx % H;
+  const int32_t b = bh_idx / H;
 
+  Walk w;
+  w.seg.l1 = a.seg_l0[1];
+  w.seg.l2 = a.seg_l0[2];
+  w.seg.l3 = a.seg_l0[3];
+  w.seg.r0 = a.seg_row0[0];
+  w.seg.r1 = a.seg_row0[1];
+  w.seg.r2 = a.seg_row0[2];
+  w.seg.r3 = a.seg_row0[3];
   // key range of this split, in whole tiles
   const int32_t tiles = (a.n_keys + kBlockK - 1) / kBlockK;
   const int32_t tiles_per = (tiles + a.splits - 1) / a.splits;
-  const int32_t k_begin = split * tiles_per * kBlockK;
-  const int32_t k_end = min(a.n_keys, (split + 1) * tiles_per * kBlockK);
+  w.k_begin = split * tiles_per * kBlockK;
+  w.k_end = min(a.n_keys, (split + 1) * tiles_per * kBlockK);
+  const int64_t bh = int64_t(bh_idx) * a.slots;
+  w.kbase = a.k_cache + bh * kHeadDim;
+  w.vbase = a.v_cache + bh * kHeadDim;
+  w.tid = tid;
+  w.col = col;
+  w.half = half;
+  // per-lane offset of the transposing V reads (see lds_read_tr): group g = lane >> 4,
+  // source row 4 * half + e, columns 16 * (g & 1) + 4 q
+  w.vsrc = (4 * half + ((lane & 15) >> 2)) * kVStride + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
+  w.c2 = a.scale * kLog2e;
 
-  // Q^T fragments: for d-step s, this lane holds q[qc][16 s + 8 half .. +8]
-  bf16x8_t qf[8];
-  {
-    const uint16_t* qp = a.q + ((int64_t(b) * a.N + qc) * a.H + h) * kHeadDim + 8 * half;
+  // Q^T fragments: for query block qb and d-step s, q[query][16 s + 8 half .. +8]
+  const int32_t q0 = qt * kBlockQ + wave * kQPerWave;
+  bf16x8_t qf[kQB][8];
 #pragma unroll
-    for (int s = 0; s < 8; ++s) qf[s] = as_bf16x8(*reinterpret_cast<const uint4*>(qp + 16 * s));
+  for (int qb = 0; qb < kQB; ++qb) {
+    const int32_t qi = q0 + qb * 32 + col;
+    const int32_t qc = qi < N ? qi : N - 1;
+    const uint16_t* qp = a.q + ((int64_t(b) * N + qc) * H + h) * kHeadDim + 8 * half;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) qf[qb][s] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(qp + 16 * s));
   }
 
-  const int64_t bh = (int64_t(b) * a.H + h) * a.slots;
-  const uint16_t* kbase = a.k_cache + bh * kHeadDim;
-  const uint16_t* vbase = a.v_cache + bh * kHeadDim;
-  const float c2 = a.scale * kLog2e;
-
-  f32x16_t o[4];
+  // Pass 0: each row's exponent offset is the max of the range's first key tile, so later
+  // probabilities may exceed 1.  If a row's sum exceeds 2^64 (its scores grew by more than
+  // 64 / (scale log2 e) after the first tile), the work-group redoes its range with the
+  // exact row max, where no probability exceeds 1.
+  f32x16_t o[kQB][4];
+  float m_off[kQB];
+  float l_run[kQB];
 #pragma unroll
-  for (int d = 0; d < 4; ++d)
+  for (int qb = 0; qb < kQB; ++qb) m_off[qb] = 0.f;
+  attend<true>(sm, w, qf, m_off, o, l_run);
+  bool overflow = false;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) o[d][i] = 0.f;
-  float m_run = -INFINITY;
-  float l_run = 0.f;
-
-  for (int32_t kt0 = k_begin; kt0 < k_end; kt0 += kBlockK) {
-    __syncthreads();
-    // ---- stage K (row-major) and V^T into LDS
-#pragma unroll
-    for (int j = 0; j < (kBlockK * kHeadDim / 8) / kThreads; ++j) {
-      const int chunk = tid + kThreads * j;
-      const int row = chunk >> 4;
-      const int piece = chunk & 15;
-      const int32_t key = kt0 + row;
-      uint4 kx = make_uint4(0, 0, 0, 0), vx = make_uint4(0, 0, 0, 0);
-      if (key < k_end) {
-        const int64_t off = int64_t(key_row(a, key)) * kHeadDim + piece * 8;
-        kx = *reinterpret_cast<const uint4*>(kbase + off);
-        vx = *reinterpret_cast<const uint4*>(vbase + off);
-      }
-      *reinterpret_cast<uint4*>(&sm.k[row * kKStride + piece * 8]) = kx;
-      const uint32_t w[4] = {vx.x, vx.y, vx.z, vx.w};
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        sm.vt[(piece * 8 + 2 * e) * kVStride + row] = uint16_t(w[e] & 0xffffu);
-        sm.vt[(piece * 8 + 2 * e + 1) * kVStride + row] = uint16_t(w[e] >> 16);
-      }
-    }
-    __syncthreads();
-
-    // ---- S^T = K * Q^T for two 32-key blocks
-    f32x16_t s[2];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-      for (int i = 0; i < 16; ++i) s[kb][i] = 0.f;
-#pragma unroll
-      for (int st = 0; st < 8; ++st) {
-        const bf16x8_t kf = as_bf16x8(
-            *reinterpret_cast<const uint4*>(&sm.k[(kb * 32 + col) * kKStride + 16 * st + 8 * half]));
-        s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[st], s[kb], 0, 0, 0);
-      }
-    }
-
-    // ---- mask keys past the range (last tile only)
-    if (kt0 + kBlockK > k_end) {
-#pragma unroll
-      for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int32_t key = kt0 + kb * 32 + 8 * (i >> 2) + 4 * half + (i & 3);
-          if (key >= k_end) s[kb][i] = -INFINITY;
-        }
-    }
-
-    // ---- online softmax (this lane: one query, 32 keys; partner lane: the other 32)
-    float mx = s[0][0];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, s[kb][i]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float m_new = fmaxf(m_run, mx);
-    const float alpha = __builtin_amdgcn_exp2f((m_run - m_new) * c2);
-    const float moff = m_new * c2;
-    float psum = 0.f;
-    bf16x8_t pf[4];
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(s[kb][i], c2, -moff));
-        psum += p;
-        pf[kb * 2 + (i >> 3)][i & 7] = (__bf16)p;
-      }
-    l_run = l_run * alpha + psum;
-    m_run = m_new;
-#pragma unroll
-    for (int d = 0; d < 4; ++d)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) o[d][i] *= alpha;
-
-    // ---- O^T += V^T * P^T, four 16-key steps
-#pragma unroll
-    for (int t = 0; t < 4; ++t) {
-#pragma unroll
-      for (int d = 0; d < 4; ++d) {
-        const uint16_t* vp = &sm.vt[(d * 32 + col) * kVStride + 16 * t + 4 * half];
-        const uint2 lo = *reinterpret_cast<const uint2*>(vp);
-        const uint2 hi = *reinterpret_cast<const uint2*>(vp + 8);
-        const bf16x8_t vf = as_bf16x8(make_uint4(lo.x, lo.y, hi.x, hi.y));
-        o[d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[t], o[d], 0, 0, 0);
-      }
-    }
+  for (int qb = 0; qb < kQB; ++qb) overflow = overflow || !(l_run[qb] <= 0x1p64f);
+  if (__syncthreads_or(overflow)) {
+    exact_row_max(sm, w, qf, m_off);
+    attend<false>(sm, w, qf, m_off, o, l_run);
   }
 
   // ---- epilogue
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
-  if (a.splits == 1) {
-    if (qi < a.N) {
+#pragma unroll
+  for (int qb = 0; qb < kQB; ++qb) {
+    const int32_t qi = q0 + qb * 32 + col;
+    const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32);
+    if (qi >= N) continue;
+    if (a.splits == 1) {
       const float inv = 1.f / l_tot;
-      uint16_t* op = a.out + ((int64_t(b) * a.N + qi) * a.H + h) * kHeadDim + 4 * half;
+      uint16_t* op = a.out + ((int64_t(b) * N + qi) * H + h) * kHeadDim + 4 * half;
 #pragma unroll
       for (int d = 0; d < 4; ++d)
 #pragma unroll
@@ -199,26 +370,24 @@ __global__ __launch_bounds__(kThreads, 2) void window_attn_kernel(AttnArgs a) {
           typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
           bf16x4_t r;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) r[e] = (__bf16)(o[d][4 * g + e] * inv);
+          for (int e = 0; e < 4; ++e) r[e] = (__bf16)(o[qb][d][4 * g + e] * inv);
           *reinterpret_cast<bf16x4_t*>(op + d * 32 + 8 * g) = r;
         }
-      if (a.lse && half == 0) a.lse[(int64_t(b) * a.H + h) * a.N + qi] = m_run * a.scale + logf(l_tot);
-    }
-  } else {
-    if (qi < a.N) {
-      const int64_t row = ((int64_t(split) * a.B + b) * a.H + h) * a.N + qi;
+      if (a.lse && half == 0) a.lse[(int64_t(b) * H + h) * N + qi] = m_off[qb] * a.scale + logf(l_tot);
+    } else {
+      const int64_t row = ((int64_t(split) * a.B + b) * H + h) * N + qi;
       const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
       float* op = a.part_o + row * kHeadDim + 4 * half;
 #pragma unroll
       for (int d = 0; d < 4; ++d)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          float4 r = make_float4(o[d][4 * g] * inv, o[d][4 * g + 1] * inv, o[d][4 * g + 2] * inv,
-                                 o[d][4 * g + 3] * inv);
+          const float4 r = make_float4(o[qb][d][4 * g] * inv, o[qb][d][4 * g + 1] * inv, o[qb][d][4 * g + 2] * inv,
+                                       o[qb][d][4 * g + 3] * inv);
           *reinterpret_cast<float4*>(op + d * 32 + 8 * g) = r;
         }
       if (half == 0) {
-        a.part_ml[row * 2] = m_run;
+        a.part_ml[row * 2] = l_tot > 0.f ? m_off[qb] : -INFINITY;
         a.part_ml[row * 2 + 1] = l_tot;
       }
     }
@@ -267,11 +436,11 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
 }  // namespace
 
 int32_t attn_choose_splits(int32_t B, int32_t H, int32_t N, int32_t n_keys) {
-  // Estimated time of s splits: rounds of resident work-groups (256 compute units x 2)
+  // Estimated time of s splits: rounds of resident work-groups (one per compute unit)
   // times the key tiles each work-group walks, plus the combine's traffic (partials
   // written and read back, fp32) at a sustained 5 TB/s.  A split keeps >= 4 tiles.
-  constexpr int64_t kSlots = 256 * 2;
-  constexpr double kTileUs = 2.0;             // one 128-query x 64-key tile per work-group
+  constexpr int64_t kSlots = 256 * kGroupsPerCU;
+  constexpr double kTileUs = 1.7 * kQB;       // one work-group's 64-key tile
   constexpr double kBytesPerUs = 5.0e6;
   const int64_t groups = int64_t(B) * H * ((N + kBlockQ - 1) / kBlockQ);
   const int32_t tiles = (n_keys + kBlockK - 1) / kBlockK;
@@ -300,7 +469,7 @@ size_t attn_workspace_bytes(int32_t B, int32_t H, int32_t N, int32_t splits) {
 }
 
 hipError_t launch_window_attn(const AttnArgs& a, hipStream_t stream) {
-  dim3 grid(unsigned((a.N + kBlockQ - 1) / kBlockQ), unsigned(a.H), unsigned(a.B * a.splits));
+  dim3 grid(unsigned(int64_t((a.N + kBlockQ - 1) / kBlockQ) * a.H * a.B * a.splits));
   hipLaunchKernelGGL(window_attn_kernel, grid, dim3(kThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.splits == 1) return e;

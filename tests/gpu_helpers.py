@@ -22,6 +22,10 @@ MEAN_ABS = 2e-3
 # tighter relative bound: bf16 rounding of the output (<= 2^-9 relative) and of the
 # probabilities fed to the PV product keep the mean error well under 2^-7 of the mean |o|
 MEAN_REL = 2.0 ** -7
+# log-sum-exp bound: the row sum is accumulated from the bf16-rounded probabilities that
+# enter the PV product (each within 2^-9 relative), so log(sum) moves by at most 2^-9 plus
+# fp32 rounding; 2^-8 leaves margin for the latter
+LSE_ABS = 2.0 ** -8
 
 
 def log(msg: str) -> None:

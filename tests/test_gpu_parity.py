@@ -16,7 +16,7 @@ import torch
 
 import synth
 from oracle import numerics
-from tests.gpu_helpers import Mirror, check_attention, dev, host, log, sample_queries
+from tests.gpu_helpers import LSE_ABS, Mirror, check_attention, dev, host, log, sample_queries
 
 pytestmark = pytest.mark.gpu
 
@@ -51,7 +51,7 @@ def test_tiny_full_compare(u):
     m.check_cache("tiny")
     want, want_lse = m.expected(q_rot_ref, wl.f0, wl.C, wl.W)
     log(f"  {check_attention(host(out), want, 'tiny')}")
-    assert np.max(np.abs(lse.cpu().numpy() - want_lse)) < 1e-4
+    assert np.max(np.abs(lse.cpu().numpy() - want_lse)) <= LSE_ABS
 
 
 @pytest.mark.parametrize("use_split", [True, False])
@@ -68,7 +68,7 @@ def test_full_chunk(u, use_split):
     idx = sample_queries(wl.n_query, 192, 7)
     want, want_lse = m.expected(q_rot_ref, wl.f0, wl.C, wl.W, query_idx=idx)
     log(f"  {check_attention(host(out)[:, idx], want, 'full_chunk')}")
-    assert np.max(np.abs(lse.cpu().numpy()[:, :, idx] - want_lse)) < 1e-4
+    assert np.max(np.abs(lse.cpu().numpy()[:, :, idx] - want_lse)) <= LSE_ABS
 
 
 def test_unwindowed(u):
@@ -155,7 +155,7 @@ def test_ragged_batch2_sinks_fused_qkv(u, use_split):
         m.check_cache(f"ragged chunk {f0}")
         want, want_lse = m.expected(q_rot_ref, f0, 2, 13)
         check_attention(host(out), want, f"ragged chunk {f0}")
-        assert np.max(np.abs(lse.cpu().numpy() - want_lse)) < 1e-4
+        assert np.max(np.abs(lse.cpu().numpy() - want_lse)) <= LSE_ABS
 
 
 def test_refine_overwrites_in_place(u):
