@@ -46,6 +46,9 @@ def parse():
     p.add_argument("--sets", type=int, default=4)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-queries", type=int, default=2048, help="oracle sample: queries x all heads")
+    p.add_argument("--copy-calibration", type=int, default=0, metavar="MB",
+                   help="only run a plain device-to-device copy of MB megabytes (x5), for scaling HBM "
+                        "byte counters read by a profiler")
     return p.parse_args()
 
 
@@ -204,6 +207,15 @@ def main():
     if not torch.cuda.is_available():
         print("bench.py: no GPU visible", file=sys.stderr)
         sys.exit(1)
+    if args.copy_calibration:
+        n = args.copy_calibration * 1000 * 1000
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": n, "copies": 5}), flush=True)
+        return
     import paper_2609_32518_amd as u
 
     wl = synth.WORKLOADS[args.workload]

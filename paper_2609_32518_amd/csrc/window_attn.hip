@@ -39,20 +39,12 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
 constexpr int kBlockK = 64;                   // keys per tile
-#ifndef UNSTEP_ATTN_QB
-#define UNSTEP_ATTN_QB 1
-#endif
-// 32-query blocks per wave: 1 -> 128 queries per work-group and two work-groups per
-// compute unit (two waves per SIMD); 2 -> 256 queries per work-group, one wave per SIMD.
-constexpr int kQB = UNSTEP_ATTN_QB;
+constexpr int kQB = 1;                        // 32-query blocks per wave
 constexpr int kQPerWave = 32 * kQB;
-constexpr int kBlockQ = kWaves * kQPerWave;
-constexpr int kGroupsPerCU = kQB == 1 ? 2 : 1;
-// LDS row strides (bf16 elements).  K: 68 dwords, so the 16 lanes of each b128 read
-// phase (16 rows, same columns) cover all 64 banks once.  V: 80 dwords, so each half-wave
-// of a transposing b64 read (4 rows x 64 bytes) covers all 64 banks once.
-constexpr int kKStride = kHeadDim + 8;
-constexpr int kVStride = kHeadDim + 32;
+constexpr int kBlockQ = kWaves * kQPerWave;   // 128 queries per work-group
+constexpr int kGroupsPerCU = 2;               // two work-groups per compute unit
+constexpr int kRowBytes = kHeadDim * 2;       // one K or V row (bf16)
+constexpr int kTileBytes = kBlockK * kRowBytes;
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kXcds = 8;
 
@@ -63,14 +55,25 @@ typedef float f32x16_t __attribute__((ext_vector_type(16)));
 typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
 typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
 typedef __attribute__((address_space(3))) i16x4_t lds_i16x4_t;
+typedef __attribute__((address_space(3))) u32x4_t lds_u32x4_t;
+typedef __attribute__((address_space(1))) void global_void_t;
+typedef __attribute__((address_space(3))) void lds_void_t;
 
-struct Smem {
-  uint16_t k[2][kBlockK * kKStride];
-  uint16_t v[2][kBlockK * kVStride];
+// LDS: two buffers of one K tile and one V tile, rows of 256 bytes without padding, each
+// its own array so that loads into one buffer are seen not to alias reads of the other.
+// The sixteen 16-byte slots of row r are XOR-swizzled with swz(r), so that both read
+// patterns are bank-conflict free: the b128 K reads (16 lanes = 16 consecutive rows at
+// one logical slot) and the transposing V reads (per half-wave 4 consecutive rows x
+// 4 consecutive slots).
+struct Buffers {
+  uint8_t* k;
+  uint8_t* v;
 };
 
+__device__ __forceinline__ int swz(int row) { return ((row & 3) << 2) | ((row >> 2) & 3); }
+
 // Physical cache row of a logical key index: up to four runs of consecutive rows, the
-// first starting at logical index 0.  Held in scalar registers, resolved with selects.
+// first starting at logical index 0.
 struct SegTable {
   int32_t l1, l2, l3;          // logical start of runs 1..3 (INT32_MAX when absent)
   int32_t r0, r1, r2, r3;      // physical row of each run's first key
@@ -81,71 +84,69 @@ struct SegTable {
     r = key >= l3 ? r3 + (key - l3) : r;
     return r;
   }
+  // Logical start of the run after the one holding key (INT32_MAX for the last run).
+  __device__ __forceinline__ int32_t run_end(int32_t key) const {
+    return key < l1 ? l1 : key < l2 ? l2 : key < l3 ? l3 : INT32_MAX;
+  }
 };
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t u) { return __builtin_bit_cast(bf16x8_t, u); }
 
 // Transposing LDS read: within each 16-lane group, lane i receives element (i & 3) of
 // the 4 x b16 rows addressed by lanes 4e + (i >> 2), e = 0..3.
-__device__ __forceinline__ u32x2_t lds_read_tr(const uint16_t* p) {
+__device__ __forceinline__ u32x2_t lds_read_tr(const uint8_t* p) {
   const i16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(p));
   return __builtin_bit_cast(u32x2_t, v);
 }
 
 // Everything one work-group needs while it walks its key range.
 struct Walk {
-  const uint16_t* kbase;       // this (batch, head)'s K rows
-  const uint16_t* vbase;
+  const uint8_t* kbase;        // this (batch, head)'s K rows
+  const uint8_t* vbase;
   SegTable seg;
   int32_t k_begin, k_end;      // logical key range
-  int tid, col, half, vsrc;
+  int wave, lane, col, half;
+  int lrow;                    // loader: tile row of this lane in its first load (+4 i)
+  int lpiece[4];               // loader: byte offset of this lane's logical 16-byte piece
+  int koff[8];                 // K fragment byte offsets for d-steps 0..7 (row = col)
+  int voff[2][4];              // V^T fragment byte offsets for (upper 8 keys, d block)
   float c2;                    // scale * log2(e)
 };
 
-// One 64-key tile's 16-byte pieces for this thread: (row, piece) = (c >> 4, c & 15),
-// c = tid + 256 j.  Keys past the range read the range's last key (finite values whose
-// scores are masked to -inf).
-struct TileRegs {
-  u32x4_t k0, k1, k2, k3;
-  u32x4_t v0, v1, v2, v3;
-};
-
-__device__ __forceinline__ void load_piece(u32x4_t& kx, u32x4_t& vx, const Walk& w, int32_t kt0, int j) {
-  const int c = w.tid + kThreads * j;
-  const int32_t key = min(kt0 + (c >> 4), w.k_end - 1);
-  const int64_t off = int64_t(w.seg.row(key)) * kHeadDim + (c & 15) * 8;
-  kx = *reinterpret_cast<const u32x4_t*>(w.kbase + off);
-  vx = *reinterpret_cast<const u32x4_t*>(w.vbase + off);
+// Direct-to-LDS load of one 64-key tile of K and V into buffer `buf`.  Wave w loads tile
+// rows 16 w .. 16 w + 15 in four 1 KB instructions; lane l of instruction i lands in
+// row 16 w + 4 i + (l >> 4), physical slot l & 15, and so fetches logical piece
+// (l & 15) ^ swz(row).  Keys past the range read the range's last key (finite values;
+// their scores are masked to -inf).
+__device__ __forceinline__ void load_tile(Buffers bf, const Walk& w, int32_t kt0) {
+  int32_t rows[4];
+  const int32_t run_end = w.seg.run_end(kt0);
+  if (kt0 + kBlockK <= min(run_end, w.k_end)) {      // whole tile inside one run
+    const int32_t base = w.seg.row(kt0);
+#pragma unroll
+    for (int i = 0; i < 4; ++i) rows[i] = base + w.lrow + 4 * i;
+  } else {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) rows[i] = w.seg.row(min(kt0 + w.lrow + 4 * i, w.k_end - 1));
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t off = uint32_t(rows[i]) * kRowBytes + w.lpiece[i];
+    uint8_t* kd = bf.k + (16 * w.wave + 4 * i) * kRowBytes;
+    uint8_t* vd = bf.v + (16 * w.wave + 4 * i) * kRowBytes;
+    __builtin_amdgcn_global_load_lds((global_void_t*)(w.kbase + off), (lds_void_t*)kd, 16, 0, 0);
+    __builtin_amdgcn_global_load_lds((global_void_t*)(w.vbase + off), (lds_void_t*)vd, 16, 0, 0);
+  }
 }
 
-__device__ __forceinline__ void load_tile(TileRegs& r, const Walk& w, int32_t kt0) {
-  load_piece(r.k0, r.v0, w, kt0, 0);
-  load_piece(r.k1, r.v1, w, kt0, 1);
-  load_piece(r.k2, r.v2, w, kt0, 2);
-  load_piece(r.k3, r.v3, w, kt0, 3);
-}
-
-__device__ __forceinline__ void store_piece(Smem& sm, int buf, const u32x4_t& kx, const u32x4_t& vx, int tid, int j) {
-  const int c = tid + kThreads * j;
-  *reinterpret_cast<u32x4_t*>(&sm.k[buf][(c >> 4) * kKStride + (c & 15) * 8]) = kx;
-  *reinterpret_cast<u32x4_t*>(&sm.v[buf][(c >> 4) * kVStride + (c & 15) * 8]) = vx;
-}
-
-__device__ __forceinline__ void store_tile(Smem& sm, int buf, const TileRegs& r, int tid) {
-  store_piece(sm, buf, r.k0, r.v0, tid, 0);
-  store_piece(sm, buf, r.k1, r.v1, tid, 1);
-  store_piece(sm, buf, r.k2, r.v2, tid, 2);
-  store_piece(sm, buf, r.k3, r.v3, tid, 3);
-}
-
-// S^T for key block kb of the tile in LDS: both 32-query blocks share each K fragment.
-__device__ __forceinline__ void qk_block(f32x16_t (&s)[kQB], const uint16_t* kt, const bf16x8_t (&qf)[kQB][8], int kb,
+// S^T for key block kb of the tile in LDS.
+__device__ __forceinline__ void qk_block(f32x16_t (&s)[kQB], const uint8_t* kt, const bf16x8_t (&qf)[kQB][8], int kb,
                                          const Walk& w) {
   const f32x16_t zero = {};
+  const uint8_t* kr = kt + kb * 32 * kRowBytes;
 #pragma unroll
   for (int st = 0; st < 8; ++st) {
-    const bf16x8_t kf =
-        as_bf16x8(*reinterpret_cast<const u32x4_t*>(&kt[(kb * 32 + w.col) * kKStride + 16 * st + 8 * w.half]));
+    const bf16x8_t kf = as_bf16x8(*(const lds_u32x4_t*)(kr + w.koff[st]));
 #pragma unroll
     for (int qb = 0; qb < kQB; ++qb)
       s[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][st], st == 0 ? zero : s[qb], 0, 0, 0);
@@ -163,7 +164,7 @@ __device__ __forceinline__ void mask_block(f32x16_t (&s)[kQB], int32_t key0, int
 // Probabilities (bf16) of key block kb and their row sums, then O^T += V^T * P^T over
 // the block's two 16-key steps.
 __device__ __forceinline__ void pv_block(f32x16_t (&o)[kQB][4], float (&l)[kQB], const f32x16_t (&s)[kQB],
-                                         const uint16_t* vt, int kb, const float (&m_off)[kQB], const Walk& w) {
+                                         const uint8_t* vt, int kb, const float (&m_off)[kQB], const Walk& w) {
   const bf16x2_t ones = {(__bf16)1.f, (__bf16)1.f};
   bf16x8_t pf[kQB][2];
 #pragma unroll
@@ -183,11 +184,11 @@ __device__ __forceinline__ void pv_block(f32x16_t (&o)[kQB][4], float (&l)[kQB],
   }
 #pragma unroll
   for (int sub = 0; sub < 2; ++sub) {
-    const int t = kb * 2 + sub;
+    const uint8_t* vr = vt + (32 * kb + 16 * sub) * kRowBytes;
 #pragma unroll
     for (int d = 0; d < 4; ++d) {
-      const u32x2_t lo = lds_read_tr(vt + (16 * t) * kVStride + 32 * d);
-      const u32x2_t hi = lds_read_tr(vt + (16 * t + 8) * kVStride + 32 * d);
+      const u32x2_t lo = lds_read_tr(vr + w.voff[0][d]);
+      const u32x2_t hi = lds_read_tr(vr + w.voff[1][d]);
       const bf16x8_t vf = as_bf16x8(u32x4_t{lo.x, lo.y, hi.x, hi.y});
 #pragma unroll
       for (int qb = 0; qb < kQB; ++qb)
@@ -199,9 +200,38 @@ __device__ __forceinline__ void pv_block(f32x16_t (&o)[kQB][4], float (&l)[kQB],
 // Walk the key range once with fixed per-row exponent offsets m_off (raw score units).
 // kFromFirstTile: set m_off from the first tile's row max (pass 0); otherwise m_off is
 // given (the exact row max).  Accumulates O^T (o) and the row sums (l) from zero.
+// One tile: S^T, masking, (first tile: offsets), then P and O^T, from buffer `cur`.
 template <bool kFromFirstTile>
-__device__ __forceinline__ void attend(Smem& sm, const Walk& w, const bf16x8_t (&qf)[kQB][8], float (&m_off)[kQB],
-                                       f32x16_t (&o)[kQB][4], float (&l)[kQB]) {
+__device__ __forceinline__ void attend_tile(Buffers cur, const Walk& w, int32_t kt0, const bf16x8_t (&qf)[kQB][8],
+                                            float (&m_off)[kQB], f32x16_t (&o)[kQB][4], float (&l)[kQB]) {
+  f32x16_t s0[kQB], s1[kQB];
+  qk_block(s0, cur.k, qf, 0, w);
+  qk_block(s1, cur.k, qf, 1, w);
+  if (kt0 + kBlockK > w.k_end) {
+    mask_block(s0, kt0, w.k_end, w.half);
+    mask_block(s1, kt0 + 32, w.k_end, w.half);
+  }
+  if (kFromFirstTile && kt0 == w.k_begin) {
+#pragma unroll
+    for (int qb = 0; qb < kQB; ++qb) {
+      float m = s0[qb][0];
+#pragma unroll
+      for (int i = 0; i < 16; ++i) m = fmaxf(fmaxf(m, s0[qb][i]), s1[qb][i]);
+      m_off[qb] = fmaxf(m, __shfl_xor(m, 32));
+    }
+  }
+  pv_block(o, l, s0, cur.v, 0, m_off, w);
+  pv_block(o, l, s1, cur.v, 1, m_off, w);
+}
+
+// Walk the key range once with fixed per-row exponent offsets m_off (raw score units).
+// kFromFirstTile: set m_off from the first tile's row max (pass 0); otherwise m_off is
+// given (the exact row max).  Accumulates O^T (o) and the row sums (l) from zero.
+// Tiles alternate between buffers b0 and b1; while one is read, the next tile is loaded
+// into the other.
+template <bool kFromFirstTile>
+__device__ __forceinline__ void attend(Buffers b0, Buffers b1, const Walk& w, const bf16x8_t (&qf)[kQB][8],
+                                       float (&m_off)[kQB], f32x16_t (&o)[kQB][4], float (&l)[kQB]) {
   const f32x16_t zero = {};
 #pragma unroll
   for (int qb = 0; qb < kQB; ++qb) {
@@ -209,62 +239,39 @@ __device__ __forceinline__ void attend(Smem& sm, const Walk& w, const bf16x8_t (
 #pragma unroll
     for (int d = 0; d < 4; ++d) o[qb][d] = zero;
   }
-  TileRegs pre;
-  if (w.k_begin < w.k_end) {
-    load_tile(pre, w, w.k_begin);
-    store_tile(sm, 0, pre, w.tid);
-  }
+  if (w.k_begin < w.k_end) load_tile(b0, w, w.k_begin);
+  __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
-  int buf = 0;
-  for (int32_t kt0 = w.k_begin; kt0 < w.k_end; kt0 += kBlockK, buf ^= 1) {
-    const bool has_next = kt0 + kBlockK < w.k_end;
-    if (has_next) load_tile(pre, w, kt0 + kBlockK);
-    const uint16_t* kt = sm.k[buf];
-    const uint16_t* vt = sm.v[buf] + w.vsrc;
-    const bool last = kt0 + kBlockK > w.k_end;
-
-    f32x16_t s0[kQB], s1[kQB];
-    qk_block(s0, kt, qf, 0, w);
-    qk_block(s1, kt, qf, 1, w);
-    if (last) {
-      mask_block(s0, kt0, w.k_end, w.half);
-      mask_block(s1, kt0 + 32, w.k_end, w.half);
-    }
-    if (kFromFirstTile && kt0 == w.k_begin) {
-#pragma unroll
-      for (int qb = 0; qb < kQB; ++qb) {
-        float m = s0[qb][0];
-#pragma unroll
-        for (int i = 0; i < 16; ++i) m = fmaxf(fmaxf(m, s0[qb][i]), s1[qb][i]);
-        m_off[qb] = fmaxf(m, __shfl_xor(m, 32));
-      }
-    }
-
-    pv_block(o, l, s0, vt, 0, m_off, w);
-    pv_block(o, l, s1, vt, 1, m_off, w);
-
-    if (has_next) store_tile(sm, buf ^ 1, pre, w.tid);
+  for (int32_t kt0 = w.k_begin; kt0 < w.k_end; kt0 += 2 * kBlockK) {
+    if (kt0 + kBlockK < w.k_end) load_tile(b1, w, kt0 + kBlockK);
+    attend_tile<kFromFirstTile>(b0, w, kt0, qf, m_off, o, l);
+    __builtin_amdgcn_s_waitcnt(0);     // this wave's loads of the next tile have landed
+    __syncthreads();                   // ... and everyone's; buffer b0 is free
+    const int32_t kt1 = kt0 + kBlockK;
+    if (kt1 >= w.k_end) break;
+    if (kt1 + kBlockK < w.k_end) load_tile(b0, w, kt1 + kBlockK);
+    attend_tile<false>(b1, w, kt1, qf, m_off, o, l);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
   }
 }
 
 // Exact row max of the scores over the key range (QK only), for the overflow fallback.
-__device__ __forceinline__ void exact_row_max(Smem& sm, const Walk& w, const bf16x8_t (&qf)[kQB][8],
+__device__ __forceinline__ void exact_row_max(Buffers b0, const Walk& w, const bf16x8_t (&qf)[kQB][8],
                                               float (&m_off)[kQB]) {
   float mx[kQB];
 #pragma unroll
   for (int qb = 0; qb < kQB; ++qb) mx[qb] = -INFINITY;
-  TileRegs r;
   for (int32_t kt0 = w.k_begin; kt0 < w.k_end; kt0 += kBlockK) {
     __syncthreads();
-    load_tile(r, w, kt0);
-    store_tile(sm, 0, r, w.tid);
+    load_tile(b0, w, kt0);
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
       f32x16_t s[kQB];
-      qk_block(s, sm.k[0], qf, kb, w);
+      qk_block(s, b0.k, qf, kb, w);
       mask_block(s, kt0 + 32 * kb, w.k_end, w.half);
 #pragma unroll
       for (int qb = 0; qb < kQB; ++qb)
@@ -278,11 +285,15 @@ __device__ __forceinline__ void exact_row_max(Smem& sm, const Walk& w, const bf1
 }
 
 __global__ __launch_bounds__(kThreads, kGroupsPerCU) void window_attn_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(16))) Smem sm;
+  __shared__ __attribute__((aligned(1024))) uint8_t lds_k0[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds_v0[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds_k1[kTileBytes];
+  __shared__ __attribute__((aligned(1024))) uint8_t lds_v1[kTileBytes];
+  const Buffers b0{lds_k0, lds_v0}, b1{lds_k1, lds_v1};
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int half = lane >> 5;
   const int col = lane & 31;
 
@@ -313,16 +324,34 @@ __global__ __launch_bounds__(kThreads, kGroupsPerCU) void window_attn_kernel(Att
   const int32_t tiles_per = (tiles + a.splits - 1) / a.splits;
   w.k_begin = split * tiles_per * kBlockK;
   w.k_end = min(a.n_keys, (split + 1) * tiles_per * kBlockK);
-  const int64_t bh = int64_t(bh_idx) * a.slots;
-  w.kbase = a.k_cache + bh * kHeadDim;
-  w.vbase = a.v_cache + bh * kHeadDim;
-  w.tid = tid;
+  const int64_t bh = int64_t(bh_idx) * a.slots * kHeadDim;
+  w.kbase = reinterpret_cast<const uint8_t*>(a.k_cache + bh);
+  w.vbase = reinterpret_cast<const uint8_t*>(a.v_cache + bh);
+  w.wave = wave;
+  w.lane = lane;
   w.col = col;
   w.half = half;
-  // per-lane offset of the transposing V reads (see lds_read_tr): group g = lane >> 4,
-  // source row 4 * half + e, columns 16 * (g & 1) + 4 q
-  w.vsrc = (4 * half + ((lane & 15) >> 2)) * kVStride + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
   w.c2 = a.scale * kLog2e;
+  // loader: row 16 wave + 4 i + (lane >> 4); swz of that row = ((lane >> 4) << 2) | i
+  w.lrow = 16 * wave + (lane >> 4);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) w.lpiece[i] = ((lane & 15) ^ (((lane >> 4) << 2) | i)) * 16;
+  // K fragment for d-step st: row col (+32 kb), logical slot 2 st + half
+#pragma unroll
+  for (int st = 0; st < 8; ++st) w.koff[st] = col * kRowBytes + ((2 * st + half) ^ swz(col)) * 16;
+  // V^T fragment (transposing read): lane (g = lane >> 4, e = (lane & 15) >> 2, q = lane & 3)
+  // addresses row 8 up + 4 half + e, d columns 32 d + 16 (g & 1) + 4 q .. +3
+  {
+    const int e = (lane & 15) >> 2, q = lane & 3, g = lane >> 4;
+#pragma unroll
+    for (int up = 0; up < 2; ++up)
+#pragma unroll
+      for (int d = 0; d < 4; ++d) {
+        const int row = 8 * up + 4 * half + e;
+        const int piece = 4 * d + 2 * (g & 1) + (q >> 1);
+        w.voff[up][d] = row * kRowBytes + (piece ^ swz(row)) * 16 + (q & 1) * 8;
+      }
+  }
 
   // Q^T fragments: for query block qb and d-step s, q[query][16 s + 8 half .. +8]
   const int32_t q0 = qt * kBlockQ + wave * kQPerWave;
@@ -345,13 +374,13 @@ __global__ __launch_bounds__(kThreads, kGroupsPerCU) void window_attn_kernel(Att
   float l_run[kQB];
 #pragma unroll
   for (int qb = 0; qb < kQB; ++qb) m_off[qb] = 0.f;
-  attend<true>(sm, w, qf, m_off, o, l_run);
+  attend<true>(b0, b1, w, qf, m_off, o, l_run);
   bool overflow = false;
 #pragma unroll
   for (int qb = 0; qb < kQB; ++qb) overflow = overflow || !(l_run[qb] <= 0x1p64f);
   if (__syncthreads_or(overflow)) {
-    exact_row_max(sm, w, qf, m_off);
-    attend<false>(sm, w, qf, m_off, o, l_run);
+    exact_row_max(b0, w, qf, m_off);
+    attend<false>(b0, b1, w, qf, m_off, o, l_run);
   }
 
   // ---- epilogue
