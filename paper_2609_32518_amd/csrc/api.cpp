@@ -143,15 +143,14 @@ int plan_attn(const unstep_cache* c, const unstep::CacheIndex& idx, int32_t f0, 
   }
   a->seg_l0[UNSTEP_MAX_SEGMENTS] = INT32_MAX;
   a->scale = scale > 0.f ? scale : 1.0f / std::sqrt(float(UNSTEP_HEAD_DIM));
-  int32_t splits = unstep::attn_choose_splits(c->B, c->H, N, a->n_keys);
-  const size_t need = unstep::attn_workspace_bytes(c->B, c->H, N, splits);
-  if (splits > 1 && (!workspace || ws_bytes < need)) splits = 1;
-  a->splits = splits;
-  if (splits > 1) {
-    const size_t rows = size_t(splits) * c->B * c->H * N;
+  const unstep::AttnPlan plan = unstep::attn_plan(c->B, c->H, N, a->n_keys);
+  if (plan.workspace > 0 && workspace && ws_bytes >= plan.workspace) {
+    a->groups = plan.groups;
     a->part_o = static_cast<float*>(workspace);
-    a->part_ml = static_cast<float*>(workspace) + rows * UNSTEP_HEAD_DIM;
+    a->part_ml = static_cast<float*>(workspace) + plan.part_o_floats;
   } else {
+    // one work-group per query tile over the whole key range: no scratch needed
+    a->groups = plan.plain_groups;
     a->part_o = nullptr;
     a->part_ml = nullptr;
   }
@@ -275,8 +274,7 @@ int unstep_attn_workspace_size(const unstep_cache* c, int32_t start_frame, int32
   int rc = c->idx.retained_count(start_frame, n_frames, window_frames, &frames, &why);
   if (rc != UNSTEP_OK) return fail_msg(rc, "unstep_attn_workspace_size", why);
   const int32_t N = n_frames * c->idx.T();
-  const int32_t splits = unstep::attn_choose_splits(c->B, c->H, N, frames * c->idx.T());
-  *bytes = unstep::attn_workspace_bytes(c->B, c->H, N, splits);
+  *bytes = unstep::attn_plan(c->B, c->H, N, frames * c->idx.T()).workspace;
   return ok();
 }
 

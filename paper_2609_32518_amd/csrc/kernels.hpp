@@ -38,21 +38,28 @@ struct AttnArgs {
   const uint16_t* v_cache;
   uint16_t* out;           // bf16 [B, N, H, 128]
   float* lse;              // [B, H, N] or null
-  float* part_o;           // split-key partial outputs [splits, B, H, N, 128] fp32 (or null)
-  float* part_ml;          // split-key partial (max, sum) [splits, B, H, N, 2] fp32 (or null)
+  float* part_o;           // balanced schedule: partial outputs [groups, 2, 128, 128] fp32
+  float* part_ml;          // ... and their (exponent offset, row sum) [groups, 2, 128, 2]; null
+                           // when groups equals the number of query tiles (no partials)
   int32_t B, N, H, slots;
   int32_t n_keys;          // retained keys
   int32_t n_seg;           // key segments (logical order)
-  int32_t seg_l0[UNSTEP_MAX_SEGMENTS + 1];   // logical start of each segment; [n_seg] = n_keys
+  int32_t seg_l0[UNSTEP_MAX_SEGMENTS + 1];   // logical start of each segment (INT32_MAX unused)
   int32_t seg_row0[UNSTEP_MAX_SEGMENTS];     // physical row of each segment's first key
-  int32_t splits;          // key-range splits (1 = none)
+  int32_t groups;          // work-groups sharing the (query tile, key tile) units equally
   float scale;             // softmax scale
 };
 
-// Bytes of split-key scratch for `splits` splits (0 when splits <= 1).
-size_t attn_workspace_bytes(int32_t B, int32_t H, int32_t N, int32_t splits);
-// Number of key splits the launcher chooses for this shape.
-int32_t attn_choose_splits(int32_t B, int32_t H, int32_t N, int32_t n_keys);
+// Work-groups and scratch bytes for an attention launch of this shape: either one
+// work-group per query tile (no scratch) or a balanced split over all compute units.
+struct AttnPlan {
+  int32_t groups;          // balanced work-groups (== plain_groups when not worth it)
+  size_t workspace;        // scratch bytes the balanced schedule needs (0 for plain)
+  int32_t plain_groups;    // one work-group per query tile
+  size_t part_o_floats;    // offset of the (offset, sum) array in the scratch, in floats
+};
+AttnPlan attn_plan(int32_t B, int32_t H, int32_t N, int32_t n_keys);
+size_t attn_workspace_bytes(int32_t groups);
 hipError_t launch_window_attn(const AttnArgs& a, hipStream_t stream);
 
 }  // namespace unstep

@@ -4,9 +4,9 @@
 // UNSTEP_MAX_SEGMENTS runs of consecutive cache rows, so a ring that wraps is read in
 // place: the tile loader maps each logical key index to its physical row.
 //
-// Work-group: 4 waves x 32 queries (kQB = 1; two work-groups per compute unit, so two
-// waves per SIMD from independent work-groups overlap one's MFMAs with the other's
-// softmax), optionally one of `splits` contiguous key ranges.  Per 64-key tile, per wave:
+// Work-group: 4 waves x 32 queries = one 128-query tile (two work-groups per compute
+// unit, so two waves per SIMD from independent work-groups overlap one's MFMAs with the
+// other's softmax).  Per 64-key tile, per wave:
 //   S^T = K_tile * Q^T   (v_mfma_f32_32x32x16_bf16, keys on the M side, queries on N):
 //       each lane owns one query column and 32 of the tile's keys, the partner lane
 //       l^32 the other 32, so row max and row sum are in-lane plus one exchange.
@@ -23,12 +23,16 @@
 // (see window_attn_kernel).  Row sums accumulate the bf16-rounded probabilities that
 // enter the PV product (v_dot2_f32_bf16).
 //
-// Work-groups are numbered so that consecutive logical units (same head, neighbouring
-// query tiles) land on the same XCD and share its L2 while they stream the same keys.
-// With splits > 1 each work-group writes its normalised partial output and its
-// (max, sum) to the workspace and attn_combine merges them by log-sum-exp.
+// Schedule: the (query tile, key tile) units of the launch are cut into `groups` equal
+// contiguous ranges, one per work-group (a balanced split keeps all compute units busy
+// when the query tiles alone would leave some idle).  A query tile whose key range falls
+// to several work-groups gets a normalised partial output and its (offset, row sum) from
+// each, and attn_combine merges them by log-sum-exp.  Work-groups are numbered so that
+// neighbouring ranges (same head, neighbouring query tiles) land on the same XCD and share
+// its L2 while they stream the same keys.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <climits>
 
 #include "kernels.hpp"
@@ -39,10 +43,13 @@ namespace {
 constexpr int kWaves = 4;
 constexpr int kThreads = kWaves * 64;
 constexpr int kBlockK = 64;                   // keys per tile
-constexpr int kQB = 1;                        // 32-query blocks per wave
+#ifndef UNSTEP_ATTN_QB
+#define UNSTEP_ATTN_QB 1
+#endif
+constexpr int kQB = UNSTEP_ATTN_QB;           // 32-query blocks per wave
 constexpr int kQPerWave = 32 * kQB;
-constexpr int kBlockQ = kWaves * kQPerWave;   // 128 queries per work-group
-constexpr int kGroupsPerCU = 2;               // two work-groups per compute unit
+constexpr int kBlockQ = kWaves * kQPerWave;   // queries per work-group
+constexpr int kGroupsPerCU = kQB == 1 ? 2 : 1;
 constexpr int kRowBytes = kHeadDim * 2;       // one K or V row (bf16)
 constexpr int kTileBytes = kBlockK * kRowBytes;
 constexpr float kLog2e = 1.4426950408889634f;
@@ -284,6 +291,25 @@ __device__ __forceinline__ void exact_row_max(Buffers b0, const Walk& w, const b
   __syncthreads();
 }
 
+// Unit bookkeeping of the balanced schedule: unit u = (query tile t, key tile k) =
+// t * Tk + k; work-group g owns units [start(g), start(g + 1)), start(g) = floor(g U / G).
+struct Schedule {
+  int64_t U, G;
+  int32_t Tk;
+  __device__ __forceinline__ int64_t start(int64_t g) const { return g * U / G; }
+  __device__ __forceinline__ int64_t owner(int64_t u) const { return ((u + 1) * G - 1) / U; }
+};
+
+__device__ __forceinline__ Schedule make_schedule(const AttnArgs& a, int32_t* qtiles_out) {
+  const int32_t qtiles = (a.N + kBlockQ - 1) / kBlockQ;
+  *qtiles_out = qtiles;
+  Schedule sc;
+  sc.Tk = (a.n_keys + kBlockK - 1) / kBlockK;
+  sc.U = int64_t(a.B) * a.H * qtiles * sc.Tk;
+  sc.G = a.groups;
+  return sc;
+}
+
 __global__ __launch_bounds__(kThreads, kGroupsPerCU) void window_attn_kernel(AttnArgs a) {
   __shared__ __attribute__((aligned(1024))) uint8_t lds_k0[kTileBytes];
   __shared__ __attribute__((aligned(1024))) uint8_t lds_v0[kTileBytes];
@@ -296,20 +322,16 @@ __global__ __launch_bounds__(kThreads, kGroupsPerCU) void window_attn_kernel(Att
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int half = lane >> 5;
   const int col = lane & 31;
+  const int32_t N = a.N, H = a.H;
 
-  // XCD-aware numbering: hardware work-group g runs on XCD g % 8; give each XCD a
-  // contiguous range of logical units.
+  // XCD-aware numbering: hardware work-group i runs on XCD i % 8; give each XCD a
+  // contiguous range of logical work-groups, hence of neighbouring query tiles.
   const int32_t G = gridDim.x;
   const int32_t xcd = blockIdx.x % kXcds;
-  const int32_t unit = xcd * (G / kXcds) + min(xcd, G % kXcds) + blockIdx.x / kXcds;
-  const int32_t N = a.N, H = a.H;
-  const int32_t qtiles = (N + kBlockQ - 1) / kBlockQ;
-  const int32_t qt = unit % qtiles;
-  const int32_t rest = unit / qtiles;
-  const int32_t split = rest % a.splits;
-  const int32_t bh_idx = rest / a.splits;          // b * H + h
-  const int32_t h = bh_idx % H;
-  const int32_t b = bh_idx / H;
+  const int32_t g = xcd * (G / kXcds) + min(xcd, G % kXcds) + blockIdx.x / kXcds;
+
+  int32_t qtiles;
+  const Schedule sc = make_schedule(a, &qtiles);
 
   Walk w;
   w.seg.l1 = a.seg_l0[1];
@@ -319,14 +341,6 @@ __global__ __launch_bounds__(kThreads, kGroupsPerCU) void window_attn_kernel(Att
   w.seg.r1 = a.seg_row0[1];
   w.seg.r2 = a.seg_row0[2];
   w.seg.r3 = a.seg_row0[3];
-  // key range of this split, in whole tiles
-  const int32_t tiles = (a.n_keys + kBlockK - 1) / kBlockK;
-  const int32_t tiles_per = (tiles + a.splits - 1) / a.splits;
-  w.k_begin = split * tiles_per * kBlockK;
-  w.k_end = min(a.n_keys, (split + 1) * tiles_per * kBlockK);
-  const int64_t bh = int64_t(bh_idx) * a.slots * kHeadDim;
-  w.kbase = reinterpret_cast<const uint8_t*>(a.k_cache + bh);
-  w.vbase = reinterpret_cast<const uint8_t*>(a.v_cache + bh);
   w.wave = wave;
   w.lane = lane;
   w.col = col;
@@ -342,167 +356,198 @@ __global__ __launch_bounds__(kThreads, kGroupsPerCU) void window_attn_kernel(Att
   // V^T fragment (transposing read): lane (g = lane >> 4, e = (lane & 15) >> 2, q = lane & 3)
   // addresses row 8 up + 4 half + e, d columns 32 d + 16 (g & 1) + 4 q .. +3
   {
-    const int e = (lane & 15) >> 2, q = lane & 3, g = lane >> 4;
+    const int e = (lane & 15) >> 2, q = lane & 3, g16 = lane >> 4;
 #pragma unroll
     for (int up = 0; up < 2; ++up)
 #pragma unroll
       for (int d = 0; d < 4; ++d) {
         const int row = 8 * up + 4 * half + e;
-        const int piece = 4 * d + 2 * (g & 1) + (q >> 1);
+        const int piece = 4 * d + 2 * (g16 & 1) + (q >> 1);
         w.voff[up][d] = row * kRowBytes + (piece ^ swz(row)) * 16 + (q & 1) * 8;
       }
   }
 
-  // Q^T fragments: for query block qb and d-step s, q[query][16 s + 8 half .. +8]
-  const int32_t q0 = qt * kBlockQ + wave * kQPerWave;
-  bf16x8_t qf[kQB][8];
-#pragma unroll
-  for (int qb = 0; qb < kQB; ++qb) {
-    const int32_t qi = q0 + qb * 32 + col;
-    const int32_t qc = qi < N ? qi : N - 1;
-    const uint16_t* qp = a.q + ((int64_t(b) * N + qc) * H + h) * kHeadDim + 8 * half;
-#pragma unroll
-    for (int s = 0; s < 8; ++s) qf[qb][s] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(qp + 16 * s));
-  }
+  // Segments (query tile, key-tile range) of this work-group's unit range, walked from
+  // the last to the first: every work-group then starts at the first key tile of a query
+  // tile, so work-groups stream the same keys at about the same time (shared L2).
+  const int64_t u_begin = sc.start(g);
+  for (int64_t u_hi = sc.start(int64_t(g) + 1); u_hi > u_begin;) {
+    // segment: query tile t, key tiles [k0, k1)
+    const int64_t t = (u_hi - 1) / sc.Tk;
+    const int64_t u_lo = max<int64_t>(u_begin, t * sc.Tk);
+    const int32_t k0 = int32_t(u_lo - t * sc.Tk);
+    const int32_t k1 = int32_t(u_hi - t * sc.Tk);
+    const int slot = u_lo == u_begin ? 0 : 1;
+    const bool full = k0 == 0 && k1 == sc.Tk;
+    u_hi = u_lo;
 
-  // Pass 0: each row's exponent offset is the max of the range's first key tile, so later
-  // probabilities may exceed 1.  If a row's sum exceeds 2^64 (its scores grew by more than
-  // 64 / (scale log2 e) after the first tile), the work-group redoes its range with the
-  // exact row max, where no probability exceeds 1.
-  f32x16_t o[kQB][4];
-  float m_off[kQB];
-  float l_run[kQB];
-#pragma unroll
-  for (int qb = 0; qb < kQB; ++qb) m_off[qb] = 0.f;
-  attend<true>(b0, b1, w, qf, m_off, o, l_run);
-  bool overflow = false;
-#pragma unroll
-  for (int qb = 0; qb < kQB; ++qb) overflow = overflow || !(l_run[qb] <= 0x1p64f);
-  if (__syncthreads_or(overflow)) {
-    exact_row_max(b0, w, qf, m_off);
-    attend<false>(b0, b1, w, qf, m_off, o, l_run);
-  }
+    const int32_t qt = int32_t(t % qtiles);
+    const int32_t bh_idx = int32_t(t / qtiles);      // b * H + h
+    const int32_t h = bh_idx % H;
+    const int32_t b = bh_idx / H;
+    const int64_t bh = int64_t(bh_idx) * a.slots * kHeadDim;
+    w.kbase = reinterpret_cast<const uint8_t*>(a.k_cache + bh);
+    w.vbase = reinterpret_cast<const uint8_t*>(a.v_cache + bh);
+    w.k_begin = k0 * kBlockK;
+    w.k_end = min(a.n_keys, k1 * kBlockK);
 
-  // ---- epilogue
+    // Q^T fragments: for query block qb and d-step s, q[query][16 s + 8 half .. +8]
+    const int32_t q0 = qt * kBlockQ + wave * kQPerWave;
+    bf16x8_t qf[kQB][8];
 #pragma unroll
-  for (int qb = 0; qb < kQB; ++qb) {
-    const int32_t qi = q0 + qb * 32 + col;
-    const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32);
-    if (qi >= N) continue;
-    if (a.splits == 1) {
-      const float inv = 1.f / l_tot;
-      uint16_t* op = a.out + ((int64_t(b) * N + qi) * H + h) * kHeadDim + 4 * half;
+    for (int qb = 0; qb < kQB; ++qb) {
+      const int32_t qi = q0 + qb * 32 + col;
+      const int32_t qc = qi < N ? qi : N - 1;
+      const uint16_t* qp = a.q + ((int64_t(b) * N + qc) * H + h) * kHeadDim + 8 * half;
 #pragma unroll
-      for (int d = 0; d < 4; ++d)
+      for (int s = 0; s < 8; ++s) qf[qb][s] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(qp + 16 * s));
+    }
+
+    // Pass 0: each row's exponent offset is the max of the range's first key tile, so
+    // later probabilities may exceed 1.  If a row's sum exceeds 2^64 (its scores grew by
+    // more than 64 / (scale log2 e) after the first tile), the work-group redoes the
+    // segment with the exact row max, where no probability exceeds 1.
+    f32x16_t o[kQB][4];
+    float m_off[kQB];
+    float l_run[kQB];
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
-          bf16x4_t r;
+    for (int qb = 0; qb < kQB; ++qb) m_off[qb] = 0.f;
+    attend<true>(b0, b1, w, qf, m_off, o, l_run);
+    bool overflow = false;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) r[e] = (__bf16)(o[qb][d][4 * g + e] * inv);
-          *reinterpret_cast<bf16x4_t*>(op + d * 32 + 8 * g) = r;
+    for (int qb = 0; qb < kQB; ++qb) overflow = overflow || !(l_run[qb] <= 0x1p64f);
+    if (__syncthreads_or(overflow)) {
+      exact_row_max(b0, w, qf, m_off);
+      attend<false>(b0, b1, w, qf, m_off, o, l_run);
+    }
+
+    // ---- segment epilogue: the final output, or a partial for the combine pass
+#pragma unroll
+    for (int qb = 0; qb < kQB; ++qb) {
+      const int32_t r = wave * kQPerWave + qb * 32 + col;       // row within the query tile
+      const int32_t qi = qt * kBlockQ + r;
+      const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32);
+      if (qi >= N) continue;
+      if (full) {
+        const float inv = 1.f / l_tot;
+        uint16_t* op = a.out + ((int64_t(b) * N + qi) * H + h) * kHeadDim + 4 * half;
+#pragma unroll
+        for (int d = 0; d < 4; ++d)
+#pragma unroll
+          for (int gg = 0; gg < 4; ++gg) {
+            typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+            bf16x4_t rr;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) rr[e] = (__bf16)(o[qb][d][4 * gg + e] * inv);
+            *reinterpret_cast<bf16x4_t*>(op + d * 32 + 8 * gg) = rr;
+          }
+        if (a.lse && half == 0) a.lse[(int64_t(b) * H + h) * N + qi] = m_off[qb] * a.scale + logf(l_tot);
+      } else {
+        const int64_t prow = (int64_t(g) * 2 + slot) * kBlockQ + r;
+        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+        float* op = a.part_o + prow * kHeadDim + 4 * half;
+#pragma unroll
+        for (int d = 0; d < 4; ++d)
+#pragma unroll
+          for (int gg = 0; gg < 4; ++gg) {
+            const float4 rr = make_float4(o[qb][d][4 * gg] * inv, o[qb][d][4 * gg + 1] * inv,
+                                          o[qb][d][4 * gg + 2] * inv, o[qb][d][4 * gg + 3] * inv);
+            *reinterpret_cast<float4*>(op + d * 32 + 8 * gg) = rr;
+          }
+        if (half == 0) {
+          a.part_ml[prow * 2] = l_tot > 0.f ? m_off[qb] : -INFINITY;
+          a.part_ml[prow * 2 + 1] = l_tot;
         }
-      if (a.lse && half == 0) a.lse[(int64_t(b) * H + h) * N + qi] = m_off[qb] * a.scale + logf(l_tot);
-    } else {
-      const int64_t row = ((int64_t(split) * a.B + b) * H + h) * N + qi;
-      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-      float* op = a.part_o + row * kHeadDim + 4 * half;
-#pragma unroll
-      for (int d = 0; d < 4; ++d)
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const float4 r = make_float4(o[qb][d][4 * g] * inv, o[qb][d][4 * g + 1] * inv, o[qb][d][4 * g + 2] * inv,
-                                       o[qb][d][4 * g + 3] * inv);
-          *reinterpret_cast<float4*>(op + d * 32 + 8 * g) = r;
-        }
-      if (half == 0) {
-        a.part_ml[row * 2] = l_tot > 0.f ? m_off[qb] : -INFINITY;
-        a.part_ml[row * 2 + 1] = l_tot;
       }
     }
   }
 }
 
-// Merge the splits' partial results: out = sum_s w_s o_s / sum_s w_s with
-// w_s = l_s * 2^((m_s - M) * scale * log2e), M = max_s m_s.  One thread per 4 outputs.
+// Finish every query tile whose key range was shared by several work-groups: merge their
+// partials by log-sum-exp, out = sum_p w_p o_p / sum_p w_p with w_p = l_p 2^((m_p - M) c2),
+// M = max_p m_p.  Thread = (query tile, row, 4 output columns).
 __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
-  const int64_t rows = int64_t(a.B) * a.H * a.N;
+  int32_t qtiles;
+  const Schedule sc = make_schedule(a, &qtiles);
   const int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x;
-  if (idx >= rows * (kHeadDim / 4)) return;
-  const int64_t row = idx / (kHeadDim / 4);        // (b, h, n)
-  const int part = int(idx % (kHeadDim / 4));
+  const int64_t t = idx / (kBlockQ * (kHeadDim / 4));
+  if (t >= int64_t(a.B) * a.H * qtiles) return;
+  const int32_t r = int32_t((idx / (kHeadDim / 4)) % kBlockQ);
+  const int32_t part = int32_t(idx % (kHeadDim / 4));
+  const int32_t qt = int32_t(t % qtiles);
+  const int32_t qi = qt * kBlockQ + r;
+  if (qi >= a.N) return;
+  const int64_t ua = t * sc.Tk;
+  const int64_t ga = sc.owner(ua), gb = sc.owner(ua + sc.Tk - 1);
+  if (ga == gb) return;                               // written directly by its work-group
   const float c2 = a.scale * kLog2e;
   float M = -INFINITY;
-  for (int s = 0; s < a.splits; ++s) {
-    const float l = a.part_ml[(s * rows + row) * 2 + 1];
-    if (l > 0.f) M = fmaxf(M, a.part_ml[(s * rows + row) * 2]);
+  for (int64_t g = ga; g <= gb; ++g) {
+    const int64_t prow = (g * 2 + (sc.start(g) >= ua ? 0 : 1)) * kBlockQ + r;
+    if (a.part_ml[prow * 2 + 1] > 0.f) M = fmaxf(M, a.part_ml[prow * 2]);
   }
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
   float wsum = 0.f;
-  for (int s = 0; s < a.splits; ++s) {
-    const float m = a.part_ml[(s * rows + row) * 2];
-    const float l = a.part_ml[(s * rows + row) * 2 + 1];
+  for (int64_t g = ga; g <= gb; ++g) {
+    const int64_t prow = (g * 2 + (sc.start(g) >= ua ? 0 : 1)) * kBlockQ + r;
+    const float m = a.part_ml[prow * 2];
+    const float l = a.part_ml[prow * 2 + 1];
     if (!(l > 0.f)) continue;
-    const float w = l * __builtin_amdgcn_exp2f((m - M) * c2);
-    const float4 v = *reinterpret_cast<const float4*>(a.part_o + (s * rows + row) * kHeadDim + part * 4);
-    acc.x += w * v.x; acc.y += w * v.y; acc.z += w * v.z; acc.w += w * v.w;
-    wsum += w;
+    const float wgt = l * __builtin_amdgcn_exp2f((m - M) * c2);
+    const float4 v = *reinterpret_cast<const float4*>(a.part_o + prow * kHeadDim + part * 4);
+    acc.x += wgt * v.x;
+    acc.y += wgt * v.y;
+    acc.z += wgt * v.z;
+    acc.w += wgt * v.w;
+    wsum += wgt;
   }
   const float inv = 1.f / wsum;
-  const int64_t n = row % a.N;
-  const int64_t bh = row / a.N;
-  const int64_t hh = bh % a.H, bb = bh / a.H;
+  const int32_t bh_idx = int32_t(t / qtiles);
+  const int32_t h = bh_idx % a.H, b = bh_idx / a.H;
   typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
-  bf16x4_t r;
-  r[0] = (__bf16)(acc.x * inv);
-  r[1] = (__bf16)(acc.y * inv);
-  r[2] = (__bf16)(acc.z * inv);
-  r[3] = (__bf16)(acc.w * inv);
-  *reinterpret_cast<bf16x4_t*>(a.out + ((bb * a.N + n) * a.H + hh) * kHeadDim + part * 4) = r;
-  if (a.lse && part == 0) a.lse[row] = M * a.scale + logf(wsum);
+  bf16x4_t o;
+  o[0] = (__bf16)(acc.x * inv);
+  o[1] = (__bf16)(acc.y * inv);
+  o[2] = (__bf16)(acc.z * inv);
+  o[3] = (__bf16)(acc.w * inv);
+  *reinterpret_cast<bf16x4_t*>(a.out + ((int64_t(b) * a.N + qi) * a.H + h) * kHeadDim + part * 4) = o;
+  if (a.lse && part == 0) a.lse[(int64_t(b) * a.H + h) * a.N + qi] = M * a.scale + logf(wsum);
 }
 
 }  // namespace
 
-int32_t attn_choose_splits(int32_t B, int32_t H, int32_t N, int32_t n_keys) {
-  // Estimated time of s splits: rounds of resident work-groups (one per compute unit)
-  // times the key tiles each work-group walks, plus the combine's traffic (partials
-  // written and read back, fp32) at a sustained 5 TB/s.  A split keeps >= 4 tiles.
+AttnPlan attn_plan(int32_t B, int32_t H, int32_t N, int32_t n_keys) {
+  // Plain: one work-group per query tile over its whole key range.  Balanced: 2 work-groups
+  // per compute unit (256 CUs) share all (query tile, key tile) units equally, and query
+  // tiles cut between work-groups are merged by attn_combine.  Estimated times (us): a
+  // work-group's 128-query x 64-key tile ~1.85 with two per CU; partials (fp32, written
+  // and read back) at ~5 TB/s plus ~5 us for the extra launch.
   constexpr int64_t kSlots = 256 * kGroupsPerCU;
-  constexpr double kTileUs = 1.7 * kQB;       // one work-group's 64-key tile
-  constexpr double kBytesPerUs = 5.0e6;
-  const int64_t groups = int64_t(B) * H * ((N + kBlockQ - 1) / kBlockQ);
-  const int32_t tiles = (n_keys + kBlockK - 1) / kBlockK;
-  auto cost = [&](int32_t s) {
-    const int64_t rounds = (groups * s + kSlots - 1) / kSlots;
-    const double walk = double(rounds) * double((tiles + s - 1) / s) * kTileUs;
-    const double comb = s > 1 ? double(s) * B * H * N * (kHeadDim + 2) * 4.0 * 2.0 / kBytesPerUs : 0.0;
-    return walk + comb;
-  };
-  int32_t best = 1;
-  double best_cost = cost(1);
-  for (int32_t s = 2; s <= 8 && tiles / s >= 4; ++s) {
-    const double c = cost(s);
-    if (c < best_cost) {
-      best = s;
-      best_cost = c;
-    }
-  }
-  return best;
+  constexpr double kTileUs = 1.85;
+  const int64_t qtiles = int64_t(B) * H * ((N + kBlockQ - 1) / kBlockQ);
+  const int64_t tk = (n_keys + kBlockK - 1) / kBlockK;
+  const int64_t units = qtiles * tk;
+  AttnPlan plain{int32_t(qtiles), 0, int32_t(qtiles), 0};
+  const int64_t g = std::min<int64_t>(kSlots, units / 4);
+  if (g <= qtiles) return plain;
+  const double t_plain = double((qtiles + kSlots - 1) / kSlots) * double(tk) * kTileUs;
+  const size_t ws = attn_workspace_bytes(int32_t(g));
+  const double t_bal = double((units + g - 1) / g) * kTileUs + double(ws) * 2.0 / 5.0e6 + 5.0;
+  if (t_bal >= t_plain) return plain;
+  return AttnPlan{int32_t(g), ws, int32_t(qtiles), size_t(g) * 2 * kBlockQ * kHeadDim};
 }
 
-size_t attn_workspace_bytes(int32_t B, int32_t H, int32_t N, int32_t splits) {
-  if (splits <= 1) return 0;
-  const size_t rows = size_t(splits) * B * H * N;
+size_t attn_workspace_bytes(int32_t groups) {
+  const size_t rows = size_t(groups) * 2 * kBlockQ;
   return rows * kHeadDim * sizeof(float) + rows * 2 * sizeof(float);
 }
 
 hipError_t launch_window_attn(const AttnArgs& a, hipStream_t stream) {
-  dim3 grid(unsigned(int64_t((a.N + kBlockQ - 1) / kBlockQ) * a.H * a.B * a.splits));
-  hipLaunchKernelGGL(window_attn_kernel, grid, dim3(kThreads), 0, stream, a);
+  hipLaunchKernelGGL(window_attn_kernel, dim3(unsigned(a.groups)), dim3(kThreads), 0, stream, a);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.splits == 1) return e;
-  const int64_t work = int64_t(a.B) * a.H * a.N * (kHeadDim / 4);
+  if (e != hipSuccess || a.part_o == nullptr) return e;
+  const int64_t qtiles = int64_t(a.B) * a.H * ((a.N + kBlockQ - 1) / kBlockQ);
+  const int64_t work = qtiles * kBlockQ * (kHeadDim / 4);
   hipLaunchKernelGGL(attn_combine_kernel, dim3(unsigned((work + 255) / 256)), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
