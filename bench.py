@@ -15,7 +15,8 @@ Inputs are synthetic, seeded N(0,1) bf16, resident in HBM before timing.  Severa
 buffer sets (cache + inputs + outputs) are rotated so that consecutive steps do not
 find their data in the 256 MB Infinity Cache.  W warm-up steps, then K timed steps
 between device synchronisations; per-kernel durations come from HIP events recorded
-on the stream the kernels run on, in a second loop over the same work.
+on the stream the kernels run on: each kernel of the step launched for the same calls
+back to back between two events.
 
 Prints one JSON line.
 """
@@ -44,7 +45,7 @@ def parse():
     # the GPU settles its clock under sustained MFMA load within ~20 ms: warm up past that
     p.add_argument("--warmup", type=int, default=40)
     p.add_argument("--workload", default="full_chunk")
-    p.add_argument("--sets", type=int, default=4)
+    p.add_argument("--sets", type=int, default=6)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-queries", type=int, default=2048, help="oracle sample: queries x all heads")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MB",
@@ -133,7 +134,23 @@ class Plan:
             return call_set
         return self.step_idx % len(self.sets)
 
-    def step(self, events=None):
+    def time_kernels(self, steps):
+        """Average per-step time (ms) of the appends and of the attention calls, each launched
+        for `steps` steps back to back between two HIP events on the current stream."""
+        torch, wl = self.torch, self.wl
+        out = []
+        for which in ("append", "attn"):
+            self.step_idx = 0
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(steps):
+                self.step(only=which)
+            e1.record()
+            torch.cuda.synchronize()
+            out.append(e0.elapsed_time(e1) / steps)
+        return out
+
+    def step(self, events=None, only=None):
         """Enqueue one step.  With `events` (list), record (append_start, append_end=attn_start,
         attn_end) events around each call's two kernels."""
         torch, wl = self.torch, self.wl
@@ -150,7 +167,11 @@ class Plan:
             q, k, v = s["q"][:, :N], s["k"][:, :N], s["v"][:, :N]
             q_rot, out = s["q_rot"][:, :N], s["out"][:, :N]
             ws = self.ws.get(si)
-            if events is None:
+            if only == "append":
+                s["cache"].unstep_kv_append(f0, C, q, k, v, cos_t, sin_t, q_rot=q_rot)
+            elif only == "attn":
+                s["cache"].unstep_window_attn(f0, C, W, q_rot, out=out, workspace=ws)
+            elif events is None:
                 s["cache"].unstep_step(f0, C, W, q, k, v, cos_t, sin_t, q_rot=q_rot, out=out, workspace=ws)
             else:
                 e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
@@ -235,19 +256,26 @@ def main():
     dt = time.perf_counter() - t0
     ms = dt * 1e3 / args.steps
 
-    # per-kernel durations: HIP events on the launch stream around each kernel
-    events = []
-    for _ in range(args.steps):
-        plan.step(events)
-    torch.cuda.synchronize()
-    t_app = [e0.elapsed_time(e1) * 1e3 for (e0, e1, e2, nq, nk) in events]     # us
-    t_att = [e1.elapsed_time(e2) * 1e3 for (e0, e1, e2, nq, nk) in events]
-    fl_att = [attn_flops(wl.H, nq, nk) * wl.B for (e0, e1, e2, nq, nk) in events]
-    by_app = [rope_bytes(wl.H, nq) * wl.B for (e0, e1, e2, nq, nk) in events]
-    attn_us = sum(t_att) / len(t_att)
-    app_us = sum(t_app) / len(t_app)
-    attn_tflops = sum(fl_att) / (sum(t_att) * 1e-6) / 1e12
-    rope_gbs = sum(by_app) / (sum(t_app) * 1e-6) / 1e9
+    # per-kernel durations: each kernel of the step launched `steps` times back to back (same
+    # calls, same rotating buffer sets) between two HIP events on the stream it runs on
+    if wl.name == "rolling":
+        # a stream's attention depends on the ring state its appends left: time the two
+        # kernels of each call between events around each of them instead
+        events = []
+        for _ in range(args.steps):
+            plan.step(events)
+        torch.cuda.synchronize()
+        app_ms = sum(e0.elapsed_time(e1) for (e0, e1, e2, _, _) in events) / args.steps
+        att_ms = sum(e1.elapsed_time(e2) for (e0, e1, e2, _, _) in events) / args.steps
+    else:
+        app_ms, att_ms = plan.time_kernels(args.steps)
+    per_call_flops = sum(attn_flops(wl.H, C * wl.T, plan.keys(f0, C, W)) * wl.B for (_, f0, C, W) in plan.calls)
+    per_call_bytes = sum(rope_bytes(wl.H, C * wl.T) * wl.B for (_, f0, C, W) in plan.calls)
+    ncalls = len(plan.calls)
+    attn_us = att_ms * 1e3 / ncalls
+    app_us = app_ms * 1e3 / ncalls
+    attn_tflops = per_call_flops / (att_ms * 1e-3) / 1e12
+    rope_gbs = per_call_bytes / (app_ms * 1e-3) / 1e9
 
     value = flops / (ms * 1e-3) / 1e12
     res = {
