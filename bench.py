@@ -48,6 +48,10 @@ def parse():
     p.add_argument("--sets", type=int, default=6)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--cpu-queries", type=int, default=2048, help="oracle sample: queries x all heads")
+    p.add_argument("--summarize-profile", metavar="DIR", default=None,
+                   help="read the rocprofv3 CSV output of the profiling commands under DIR (see "
+                        "profile_commands()), write profiles/<kernel>_<workload>.md and "
+                        "profiles/traffic.json, and exit")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MB",
                    help="only run a plain device-to-device copy of MB megabytes (x5), for scaling HBM "
                         "byte counters read by a profiler")
@@ -217,8 +221,128 @@ def cpu_baseline(wl, n_queries):
                       f"{len(os.sched_getaffinity(0))} host cores visible, {platform.processor() or 'cpu'}"}
 
 
+
+KERNEL_SOURCES = {
+    "window_attn_kernel": ["paper_2609_32518_amd/csrc/window_attn.hip", "paper_2609_32518_amd/csrc/kernels.hpp"],
+    "rope_append_kernel": ["paper_2609_32518_amd/csrc/rope_append.hip", "paper_2609_32518_amd/csrc/kernels.hpp"],
+}
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+
+
+def source_hash(kernel):
+    import hashlib
+    h = hashlib.sha256()
+    for f in KERNEL_SOURCES[kernel]:
+        h.update(open(os.path.join(ROOT, f), "rb").read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic(kernel, workload):
+    """HBM bytes per launch from profiles/traffic.json, if taken on the current kernel source."""
+    try:
+        rec = json.load(open(TRAFFIC_FILE))[workload][kernel]
+    except (OSError, KeyError, ValueError):
+        return None
+    if rec.get("source") != source_hash(kernel):
+        return None
+    return rec["bytes_per_launch"]
+
+
+def profile_commands(workload="full_chunk"):
+    """The profiling commands whose output --summarize-profile reads (run from the repo root,
+    after `cd /tmp && export TMPDIR=/tmp && cd -`), DIR being their common output folder."""
+    b = f"python -u bench.py --workload {workload} --steps 30 --warmup 30 --no-cpu-baseline"
+    pmc = f"python -u bench.py --workload {workload} --steps 2 --warmup 1 --sets 1 --no-cpu-baseline"
+    cal = "python -u bench.py --copy-calibration 256"
+    return [
+        ("trace", f"rocprofv3 --kernel-trace --stats -d DIR/trace -o trace --output-format csv -- {b}"),
+        ("fetch", f"rocprofv3 --pmc FETCH_SIZE -d DIR/fetch -o fetch --output-format csv -- {pmc}"),
+        ("write", f"rocprofv3 --pmc WRITE_SIZE -d DIR/write -o write --output-format csv -- {pmc}"),
+        ("copy_fetch", f"rocprofv3 --pmc FETCH_SIZE -d DIR/copy_fetch -o copy_fetch --output-format csv -- {cal}"),
+        ("copy_write", f"rocprofv3 --pmc WRITE_SIZE -d DIR/copy_write -o copy_write --output-format csv -- {cal}"),
+        ("sq", f"rocprofv3 --pmc SQ_WAVES SQ_INSTS_VALU SQ_INSTS_MFMA SQ_VALU_MFMA_BUSY_CYCLES SQ_INSTS_LDS "
+               f"SQ_LDS_BANK_CONFLICT SQ_WAIT_INST_LDS GRBM_GUI_ACTIVE -d DIR/sq -o sq --output-format csv -- {pmc}"),
+    ]
+
+
+def summarize_profile(d, workload="full_chunk"):
+    import csv
+    import re
+    from collections import defaultdict
+
+    def kname(n):
+        m = re.search(r"::(\w+_kernel)(<[^>]*>)?\(", n)
+        if m:
+            return m.group(1) + (m.group(2) or "")
+        return "copy" if "copyBuffer" in n or "copy" in n.lower() else n[:40]
+
+    def counters(name):
+        per = defaultdict(lambda: defaultdict(list))
+        for r in csv.DictReader(open(os.path.join(d, name, f"{name}_counter_collection.csv"))):
+            per[kname(r["Kernel_Name"])][r["Counter_Name"]].append(float(r["Counter_Value"]))
+        return {k: {c: sum(v) / len(v) for c, v in cs.items()} for k, cs in per.items()}
+
+    stats = list(csv.DictReader(open(os.path.join(d, "trace", "trace_kernel_stats.csv"))))
+    fetch, write = counters("fetch"), counters("write")
+    cf, cw = counters("copy_fetch"), counters("copy_write")
+    sq = counters("sq")
+    cal_bytes = 256 * 1000 * 1000
+    copy_f = max(v["FETCH_SIZE"] for k, v in cf.items() if "FETCH_SIZE" in v and v["FETCH_SIZE"] > 1000)
+    copy_w = max(v["WRITE_SIZE"] for k, v in cw.items() if "WRITE_SIZE" in v and v["WRITE_SIZE"] > 1000)
+    f_scale = cal_bytes / (copy_f * 1024)
+    w_scale = cal_bytes / (copy_w * 1024)
+    try:
+        traffic = json.load(open(TRAFFIC_FILE))
+    except (OSError, ValueError):
+        traffic = {}
+    traffic.setdefault(workload, {})
+    lines = [f"# Kernel profile — {workload} workload", "",
+             "Commands (repo root, one MI355X, after `cd /tmp && export TMPDIR=/tmp && cd -`; DIR is an "
+             "output folder; this file was written by `python bench.py --summarize-profile DIR`):", "", "```"]
+    lines += [c.replace("DIR", "gpurun_out/prof") for _, c in profile_commands(workload)]
+    lines += ["```", "", "## Kernel trace (rocprofv3 --kernel-trace --stats)", "",
+              "| kernel | calls | average µs | min µs | max µs | % of GPU time |", "|---|---|---|---|---|---|"]
+    for r in stats[:6]:
+        lines.append(f"| {kname(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.1f} |")
+    lines += ["", "## HBM traffic per dispatch (rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE)", "",
+              f"Scale factors from a plain 256 MB device copy (`--copy-calibration 256`): FETCH_SIZE read "
+              f"{copy_f:.0f} KiB -> x{f_scale:.3f}; WRITE_SIZE read {copy_w:.0f} KiB -> x{w_scale:.3f}.", "",
+              "| kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled read MB | scaled write MB | total MB |",
+              "|---|---|---|---|---|---|"]
+    for k in sorted(set(fetch) | set(write)):
+        if not k.startswith(("window_attn", "attn_combine", "rope_append")):
+            continue
+        fk, wk = fetch.get(k, {}).get("FETCH_SIZE", 0.0), write.get(k, {}).get("WRITE_SIZE", 0.0)
+        rb, wb = fk * 1024 * f_scale, wk * 1024 * w_scale
+        lines.append(f"| {k} | {fk:.0f} | {wk:.0f} | {rb / 1e6:.2f} | {wb / 1e6:.2f} | {(rb + wb) / 1e6:.2f} |")
+        base = k.split("<")[0]
+        if base in KERNEL_SOURCES and (base != "rope_append_kernel" or k.endswith("<true>")):
+            traffic[workload][base] = {"bytes_per_launch": round(rb + wb), "read_bytes": round(rb),
+                                       "write_bytes": round(wb), "source": source_hash(base)}
+    a = sq.get("window_attn_kernel")
+    if a:
+        cyc = a["GRBM_GUI_ACTIVE"] / 8
+        tiles = a["SQ_INSTS_MFMA"] / 32
+        lines += ["", "## window_attn_kernel SQ counters (per dispatch)", "",
+                  f"- waves {a['SQ_WAVES']:.0f}; MFMA instructions {a['SQ_INSTS_MFMA']:.4g} "
+                  f"(= 32 per wave per 64-key tile); MFMA busy cycles {a['SQ_VALU_MFMA_BUSY_CYCLES']:.4g}",
+                  f"- MFMA busy fraction per SIMD {a['SQ_VALU_MFMA_BUSY_CYCLES'] / (1024 * cyc):.3f} over "
+                  f"{cyc:.4g} GPU cycles (GRBM_GUI_ACTIVE / 8 XCDs)",
+                  f"- non-MFMA VALU instructions per wave-tile {(a['SQ_INSTS_VALU'] - a['SQ_INSTS_MFMA']) / tiles:.1f}; "
+                  f"LDS instructions per wave-tile {a['SQ_INSTS_LDS'] / tiles:.1f}; "
+                  f"LDS bank conflicts {a['SQ_LDS_BANK_CONFLICT']:.0f}"]
+    out = os.path.join(ROOT, "profiles", f"kernels_{workload}.md")
+    open(out, "w").write("\n".join(lines) + "\n")
+    json.dump(traffic, open(TRAFFIC_FILE, "w"), indent=1, sort_keys=True)
+    print("\n".join(lines))
+
+
 def main():
     args = parse()
+    if args.summarize_profile:
+        summarize_profile(args.summarize_profile, args.workload)
+        return
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (the step shards by head across GPUs, but no "
               f"multi-GPU path is built); got --gpus {args.gpus}", file=sys.stderr)
@@ -292,9 +416,11 @@ def main():
         "attn": {"kernel": "window_attn", "us_per_call": round(attn_us, 2), "tflops": round(attn_tflops, 2)},
         "rope_append": {"kernel": "rope_append", "us_per_call": round(app_us, 2), "gbs": round(rope_gbs, 1)},
         "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 2), "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None},
+                     "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+                     "traffic": measured_traffic("window_attn_kernel", wl.name)},
         "rope_roofline": {"bound": "hbm", "achieved": round(rope_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                          "frac": round(rope_gbs / PEAK_HBM_GBS, 4), "traffic": None},
+                          "frac": round(rope_gbs / PEAK_HBM_GBS, 4),
+                          "traffic": measured_traffic("rope_append_kernel", wl.name)},
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(wl, args.cpu_queries)
