@@ -146,18 +146,24 @@ __device__ __forceinline__ void load_tile(Buffers bf, const Walk& w, int32_t kt0
   }
 }
 
-// S^T for key block kb of the tile in LDS.
-__device__ __forceinline__ void qk_block(f32x16_t (&s)[kQB], const uint8_t* kt, const bf16x8_t (&qf)[kQB][8], int kb,
-                                         const Walk& w) {
+// S^T for both 32-key blocks of the tile in LDS: the sixteen K fragments are read first
+// (one LDS round trip), then the MFMAs consume them in order.
+__device__ __forceinline__ void qk_tile(f32x16_t (&s0)[kQB], f32x16_t (&s1)[kQB], const uint8_t* kt,
+                                        const bf16x8_t (&qf)[kQB][8], const Walk& w) {
   const f32x16_t zero = {};
-  const uint8_t* kr = kt + kb * 32 * kRowBytes;
+  bf16x8_t kf[2][8];
 #pragma unroll
   for (int st = 0; st < 8; ++st) {
-    const bf16x8_t kf = as_bf16x8(*(const lds_u32x4_t*)(kr + w.koff[st]));
-#pragma unroll
-    for (int qb = 0; qb < kQB; ++qb)
-      s[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[qb][st], st == 0 ? zero : s[qb], 0, 0, 0);
+    kf[0][st] = as_bf16x8(*(const lds_u32x4_t*)(kt + w.koff[st]));
+    kf[1][st] = as_bf16x8(*(const lds_u32x4_t*)(kt + 32 * kRowBytes + w.koff[st]));
   }
+#pragma unroll
+  for (int st = 0; st < 8; ++st)
+#pragma unroll
+    for (int qb = 0; qb < kQB; ++qb) {
+      s0[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[0][st], qf[qb][st], st == 0 ? zero : s0[qb], 0, 0, 0);
+      s1[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[1][st], qf[qb][st], st == 0 ? zero : s1[qb], 0, 0, 0);
+    }
 }
 
 __device__ __forceinline__ void mask_block(f32x16_t (&s)[kQB], int32_t key0, int32_t k_end, int half) {
@@ -204,31 +210,36 @@ __device__ __forceinline__ void pv_block(f32x16_t (&o)[kQB][4], float (&l)[kQB],
   }
 }
 
-// Walk the key range once with fixed per-row exponent offsets m_off (raw score units).
-// kFromFirstTile: set m_off from the first tile's row max (pass 0); otherwise m_off is
-// given (the exact row max).  Accumulates O^T (o) and the row sums (l) from zero.
-// One tile: S^T, masking, (first tile: offsets), then P and O^T, from buffer `cur`.
-template <bool kFromFirstTile>
+// One tile from buffer `cur`: S^T, masking of keys past the range, then P and O^T.
 __device__ __forceinline__ void attend_tile(Buffers cur, const Walk& w, int32_t kt0, const bf16x8_t (&qf)[kQB][8],
-                                            float (&m_off)[kQB], f32x16_t (&o)[kQB][4], float (&l)[kQB]) {
+                                            const float (&m_off)[kQB], f32x16_t (&o)[kQB][4], float (&l)[kQB]) {
   f32x16_t s0[kQB], s1[kQB];
-  qk_block(s0, cur.k, qf, 0, w);
-  qk_block(s1, cur.k, qf, 1, w);
+  qk_tile(s0, s1, cur.k, qf, w);
   if (kt0 + kBlockK > w.k_end) {
     mask_block(s0, kt0, w.k_end, w.half);
     mask_block(s1, kt0 + 32, w.k_end, w.half);
   }
-  if (kFromFirstTile && kt0 == w.k_begin) {
-#pragma unroll
-    for (int qb = 0; qb < kQB; ++qb) {
-      float m = s0[qb][0];
-#pragma unroll
-      for (int i = 0; i < 16; ++i) m = fmaxf(fmaxf(m, s0[qb][i]), s1[qb][i]);
-      m_off[qb] = fmaxf(m, __shfl_xor(m, 32));
-    }
-  }
   pv_block(o, l, s0, cur.v, 0, m_off, w);
   pv_block(o, l, s1, cur.v, 1, m_off, w);
+}
+
+// Row max of the scores of the tile in `cur` (the range's first tile): the exponent offsets
+// of pass 0.
+__device__ __forceinline__ void first_tile_offsets(Buffers cur, const Walk& w, int32_t kt0,
+                                                   const bf16x8_t (&qf)[kQB][8], float (&m_off)[kQB]) {
+  f32x16_t s0[kQB], s1[kQB];
+  qk_tile(s0, s1, cur.k, qf, w);
+  if (kt0 + kBlockK > w.k_end) {
+    mask_block(s0, kt0, w.k_end, w.half);
+    mask_block(s1, kt0 + 32, w.k_end, w.half);
+  }
+#pragma unroll
+  for (int qb = 0; qb < kQB; ++qb) {
+    float m = s0[qb][0];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) m = fmaxf(fmaxf(m, s0[qb][i]), s1[qb][i]);
+    m_off[qb] = fmaxf(m, __shfl_xor(m, 32));
+  }
 }
 
 // Walk the key range once with fixed per-row exponent offsets m_off (raw score units).
@@ -249,17 +260,22 @@ __device__ __forceinline__ void attend(Buffers b0, Buffers b1, const Walk& w, co
   if (w.k_begin < w.k_end) load_tile(b0, w, w.k_begin);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
+  if (kFromFirstTile && w.k_begin < w.k_end) first_tile_offsets(b0, w, w.k_begin, qf, m_off);
 
-  for (int32_t kt0 = w.k_begin; kt0 < w.k_end; kt0 += 2 * kBlockK) {
-    if (kt0 + kBlockK < w.k_end) load_tile(b1, w, kt0 + kBlockK);
-    attend_tile<kFromFirstTile>(b0, w, kt0, qf, m_off, o, l);
+  int32_t kt0 = w.k_begin;
+  for (; kt0 + kBlockK < w.k_end; kt0 += 2 * kBlockK) {
+    load_tile(b1, w, kt0 + kBlockK);
+    attend_tile(b0, w, kt0, qf, m_off, o, l);
     __builtin_amdgcn_s_waitcnt(0);     // this wave's loads of the next tile have landed
     __syncthreads();                   // ... and everyone's; buffer b0 is free
     const int32_t kt1 = kt0 + kBlockK;
-    if (kt1 >= w.k_end) break;
     if (kt1 + kBlockK < w.k_end) load_tile(b0, w, kt1 + kBlockK);
-    attend_tile<false>(b1, w, kt1, qf, m_off, o, l);
+    attend_tile(b1, w, kt1, qf, m_off, o, l);
     __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+  }
+  if (kt0 < w.k_end) {                 // odd tile count: the last tile, in b0
+    attend_tile(b0, w, kt0, qf, m_off, o, l);
     __syncthreads();
   }
 }
@@ -275,16 +291,14 @@ __device__ __forceinline__ void exact_row_max(Buffers b0, const Walk& w, const b
     load_tile(b0, w, kt0);
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
+    f32x16_t s0[kQB], s1[kQB];
+    qk_tile(s0, s1, b0.k, qf, w);
+    mask_block(s0, kt0, w.k_end, w.half);
+    mask_block(s1, kt0 + 32, w.k_end, w.half);
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-      f32x16_t s[kQB];
-      qk_block(s, b0.k, qf, kb, w);
-      mask_block(s, kt0 + 32 * kb, w.k_end, w.half);
+    for (int qb = 0; qb < kQB; ++qb)
 #pragma unroll
-      for (int qb = 0; qb < kQB; ++qb)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) mx[qb] = fmaxf(mx[qb], s[qb][i]);
-    }
+      for (int i = 0; i < 16; ++i) mx[qb] = fmaxf(mx[qb], fmaxf(s0[qb][i], s1[qb][i]));
   }
 #pragma unroll
   for (int qb = 0; qb < kQB; ++qb) m_off[qb] = fmaxf(mx[qb], __shfl_xor(mx[qb], 32));
