@@ -4,24 +4,31 @@
 // UNSTEP_MAX_SEGMENTS runs of consecutive cache rows, so a ring that wraps is read in
 // place: the tile loader maps each logical key index to its physical row.
 //
-// Work-group: 4 waves x 32 queries = one 128-query tile (two work-groups per compute
-// unit, so two waves per SIMD from independent work-groups overlap one's MFMAs with the
-// other's softmax).  Per 64-key tile, per wave:
-//   S^T = K_tile * Q^T   (v_mfma_f32_32x32x16_bf16, keys on the M side, queries on N):
-//       each lane owns one query column and 32 of the tile's keys, the partner lane
-//       l^32 the other 32, so row max and row sum are in-lane plus one exchange.
-//   O^T += V^T * P^T     (same MFMA): P^T comes straight from the S^T registers; the
-//       MFMA's 16 contraction slots per lane pair are mapped to the keys where the S^T
-//       accumulator left them, and the matching V^T fragments are read from the
-//       row-major V tile with the transposing LDS read ds_read_b64_tr_b16.
-// K and V tiles are double-buffered in LDS; the next tile's global loads are issued
-// before the current tile's MFMAs and written to the other buffer after them (one
-// barrier per tile).
-// Softmax: fp32, base-2 exponentials of (s - m) * scale * log2(e) with a fixed per-row
-// offset m (the max of the range's first tile), so the loop never rescales the output;
-// if a row's sum exceeds 2^64 the work-group redoes its range with the exact row max
-// (see window_attn_kernel).  Row sums accumulate the bf16-rounded probabilities that
-// enter the PV product (v_dot2_f32_bf16).
+// Work-group: 8 waves x 32 queries = one 256-query tile, one work-group per compute unit.
+// Waves 0-3 (group A) and 4-7 (group B) share the four SIMDs, one wave of each group per
+// SIMD, and run half a key tile apart: the work-group alternates two phases separated by
+// barriers, and in each phase one wave of a SIMD issues MFMAs while the other computes
+// the softmax of its previous tile.  Per 64-key tile t, per wave:
+//   M phase: O^T += V^T(t-1) * P^T(t-1) and S^T(t) = K(t) * Q^T   (32 MFMAs)
+//   V phase: P(t) = exp2((S(t) - m) * scale * log2(e)) in bf16, row sums   (VALU), and
+//            this wave's share of the loads of a later stage
+// Both products use v_mfma_f32_32x32x16_bf16 with keys (S^T) or head dimensions (O^T) on
+// the M side and the wave's 32 queries on N: each lane owns one query column and half of
+// the 32 rows, the partner lane l^32 the other half, so row max and row sum are in-lane
+// plus one exchange.  P^T comes straight from the S^T registers: the MFMA's 16 contraction
+// slots per lane pair are mapped to the keys where the S^T accumulator left them, and the
+// matching V^T fragments are read from the row-major V tile with the transposing LDS read
+// ds_read_b64_tr_b16.
+// LDS: a ring of four stages; stage t holds K tile t and V tile t-1 (the operands of the
+// M phase of tile t) and is loaded straight from global memory into LDS (inline-assembly
+// global_load_lds, counted by hand) three tiles ahead, each wave fetching one eighth of it
+// during its V phase, when the wave's issue slots are not needed for MFMAs.  Fragment
+// reads in the M phase run four MFMAs ahead of their use (pinned schedule).
+// Softmax: fp32, base-2 exponentials with a fixed per-row offset m (the max of the range's
+// first tile), so the loop never rescales the output; if a row's sum exceeds 2^64 the
+// work-group redoes its range with the exact row max.  Row sums add the fp32
+// probabilities with plain fp32 adds: the packed dot-product instructions would wait for
+// the other wave's MFMAs to drain.
 //
 // Schedule: the (query tile, key tile) units of the launch are cut into `groups` equal
 // contiguous ranges, one per work-group (a balanced split keeps all compute units busy
@@ -40,16 +47,13 @@
 namespace unstep {
 namespace {
 
-constexpr int kWaves = 4;
+constexpr int kWaves = 8;
 constexpr int kThreads = kWaves * 64;
 constexpr int kBlockK = 64;                   // keys per tile
-#ifndef UNSTEP_ATTN_QB
-#define UNSTEP_ATTN_QB 1
-#endif
-constexpr int kQB = UNSTEP_ATTN_QB;           // 32-query blocks per wave
-constexpr int kQPerWave = 32 * kQB;
-constexpr int kBlockQ = kWaves * kQPerWave;   // queries per work-group
-constexpr int kGroupsPerCU = kQB == 1 ? 2 : 1;
+constexpr int kBlockQ = kWaves * 32;          // queries per work-group
+constexpr int kStages = 4;                    // LDS ring
+constexpr int kAhead = kStages - 1;           // stages in flight ahead of the one in use
+constexpr int kDmaPerStage = 4;               // direct-to-LDS loads per wave per stage
 constexpr int kRowBytes = kHeadDim * 2;       // one K or V row (bf16)
 constexpr int kTileBytes = kBlockK * kRowBytes;
 constexpr float kLog2e = 1.4426950408889634f;
@@ -66,17 +70,10 @@ typedef __attribute__((address_space(3))) u32x4_t lds_u32x4_t;
 typedef __attribute__((address_space(1))) void global_void_t;
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-// LDS: two buffers of one K tile and one V tile, rows of 256 bytes without padding, each
-// its own array so that loads into one buffer are seen not to alias reads of the other.
-// The sixteen 16-byte slots of row r are XOR-swizzled with swz(r), so that both read
-// patterns are bank-conflict free: the b128 K reads (16 lanes = 16 consecutive rows at
-// one logical slot) and the transposing V reads (per half-wave 4 consecutive rows x
-// 4 consecutive slots).
-struct Buffers {
-  uint8_t* k;
-  uint8_t* v;
-};
-
+// LDS rows are 256 bytes without padding; the sixteen 16-byte slots of row r are
+// XOR-swizzled with swz(r), so that both read patterns are bank-conflict free: the b128 K
+// reads (16 lanes = 16 consecutive rows at one logical slot) and the transposing V reads
+// (per half-wave 4 consecutive rows x 4 consecutive slots).
 __device__ __forceinline__ int swz(int row) { return ((row & 3) << 2) | ((row >> 2) & 3); }
 
 // Physical cache row of a logical key index: up to four runs of consecutive rows, the
@@ -101,208 +98,251 @@ __device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t u) { return __builtin_bit_
 
 // Transposing LDS read: within each 16-lane group, lane i receives element (i & 3) of
 // the 4 x b16 rows addressed by lanes 4e + (i >> 2), e = 0..3.
-__device__ __forceinline__ u32x2_t lds_read_tr(const uint8_t* p) {
-  const i16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(p));
+__device__ __forceinline__ u32x2_t lds_read_tr(uint32_t addr) {
+  const i16x4_t v = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4_t*)(uintptr_t)(addr));
   return __builtin_bit_cast(u32x2_t, v);
 }
 
-// Everything one work-group needs while it walks its key range.
+// Workgroup barrier that also keeps the compiler from moving memory accesses across it
+// (LDS reads of a stage must not be hoisted above the barrier that publishes it).
+// The LDS reads issued before it have returned (their stage may be refilled right after).
+__device__ __forceinline__ void barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory"); }
+
+// Wait until at most n (0, 1 or 2) stages of this wave's direct-to-LDS loads are in flight.
+// The loads are issued as inline assembly (below), so the counter waits are too: the
+// compiler neither sees these loads nor may drop or relax the waits.
+__device__ __forceinline__ void wait_stages_in_flight(int n) {
+  static_assert(kDmaPerStage == 4, "vmcnt immediates assume four loads per stage");
+  if (n <= 0)
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  else if (n == 1)
+    asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+  else
+    asm volatile("s_waitcnt vmcnt(8)" ::: "memory");
+}
+
+// Per-wave state of one walk over a key range.
 struct Walk {
   const uint8_t* kbase;        // this (batch, head)'s K rows
   const uint8_t* vbase;
   SegTable seg;
   int32_t k_begin, k_end;      // logical key range
-  int wave, lane, col, half;
-  int lrow;                    // loader: tile row of this lane in its first load (+4 i)
-  int lpiece[4];               // loader: byte offset of this lane's logical 16-byte piece
-  int koff[8];                 // K fragment byte offsets for d-steps 0..7 (row = col)
-  int voff[2][4];              // V^T fragment byte offsets for (upper 8 keys, d block)
+  int32_t n;                   // tiles in the range
+  int half;
+  int lrow;                    // loader: tile row of this lane in its first load (+4)
+  int lpiece[2];               // loader: byte offset of this lane's logical 16-byte piece
+  uint32_t lds_k, lds_v;       // LDS address of ring slot 0's K tile and V tile (uniform)
+  uint32_t koff[8];            // LDS address of the K fragment for d-step 0..7 in slot 0
+  uint32_t voff[2][4];         // LDS address of the V^T fragment (upper 8 keys, d block) in slot 0
   float c2;                    // scale * log2(e)
 };
 
-// Direct-to-LDS load of one 64-key tile of K and V into buffer `buf`.  Wave w loads tile
-// rows 16 w .. 16 w + 15 in four 1 KB instructions; lane l of instruction i lands in
-// row 16 w + 4 i + (l >> 4), physical slot l & 15, and so fetches logical piece
-// (l & 15) ^ swz(row).  Keys past the range read the range's last key (finite values;
-// their scores are masked to -inf).
-__device__ __forceinline__ void load_tile(Buffers bf, const Walk& w, int32_t kt0) {
-  int32_t rows[4];
-  const int32_t run_end = w.seg.run_end(kt0);
-  if (kt0 + kBlockK <= min(run_end, w.k_end)) {      // whole tile inside one run
-    const int32_t base = w.seg.row(kt0);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) rows[i] = base + w.lrow + 4 * i;
+// Direct-to-LDS load of 8 rows (this wave's share) of the 64-key tile starting at logical
+// key kt0 into the tile at LDS address dst: lane l of instruction i lands in row lrow + 4 i,
+// physical slot l & 15, and so fetches logical piece (l & 15) ^ swz(row).  Keys past the
+// range read the range's last key (finite values; their scores are masked to -inf).
+// Written as inline assembly: M0 holds the wave's LDS destination, the lane's 16 bytes land
+// at M0 + 16 l.
+__device__ __forceinline__ void load_rows(uint32_t dst, const uint8_t* base, const Walk& w, int wave, int32_t kt0) {
+  int32_t rows[2];
+  if (kt0 + kBlockK <= min(w.seg.run_end(kt0), w.k_end)) {      // whole tile inside one run
+    const int32_t r0 = w.seg.row(kt0);
+    rows[0] = r0 + w.lrow;
+    rows[1] = r0 + w.lrow + 4;
   } else {
 #pragma unroll
-    for (int i = 0; i < 4; ++i) rows[i] = w.seg.row(min(kt0 + w.lrow + 4 * i, w.k_end - 1));
+    for (int i = 0; i < 2; ++i) rows[i] = w.seg.row(min(kt0 + w.lrow + 4 * i, w.k_end - 1));
   }
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
+  for (int i = 0; i < 2; ++i) {
     const uint32_t off = uint32_t(rows[i]) * kRowBytes + w.lpiece[i];
-    uint8_t* kd = bf.k + (16 * w.wave + 4 * i) * kRowBytes;
-    uint8_t* vd = bf.v + (16 * w.wave + 4 * i) * kRowBytes;
-    __builtin_amdgcn_global_load_lds((global_void_t*)(w.kbase + off), (lds_void_t*)kd, 16, 0, 0);
-    __builtin_amdgcn_global_load_lds((global_void_t*)(w.vbase + off), (lds_void_t*)vd, 16, 0, 0);
+    const uint32_t m0 = dst + (8 * wave + 4 * i) * kRowBytes;
+    asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "{m0}"(m0) : "memory");
   }
 }
 
-// S^T for both 32-key blocks of the tile in LDS: the sixteen K fragments are read first
-// (one LDS round trip), then the MFMAs consume them in order.
-__device__ __forceinline__ void qk_tile(f32x16_t (&s0)[kQB], f32x16_t (&s1)[kQB], const uint8_t* kt,
-                                        const bf16x8_t (&qf)[kQB][8], const Walk& w) {
-  const f32x16_t zero = {};
-  bf16x8_t kf[2][8];
-#pragma unroll
-  for (int st = 0; st < 8; ++st) {
-    kf[0][st] = as_bf16x8(*(const lds_u32x4_t*)(kt + w.koff[st]));
-    kf[1][st] = as_bf16x8(*(const lds_u32x4_t*)(kt + 32 * kRowBytes + w.koff[st]));
+// Stage t into ring slot `slot`: K tile t and V tile t - 1.  The first and last stages hold
+// only one of them; the other half is filled with a duplicate tile so that every stage
+// costs each wave the same number of loads (the in-flight accounting counts loads).
+__device__ __forceinline__ void load_stage(int slot, const Walk& w, int wave, int32_t t) {
+  const int32_t tk = min(t, w.n - 1), tv = max(t - 1, 0);
+  load_rows(w.lds_k + slot * kTileBytes, w.kbase, w, wave, w.k_begin + tk * kBlockK);
+  load_rows(w.lds_v + slot * kTileBytes, w.vbase, w, wave, w.k_begin + tv * kBlockK);
+}
+
+// Register state of one wave.
+struct Acc {
+  f32x16_t o[4];               // O^T: head dims 32 d .. 32 d + 31 x the wave's 32 queries
+  f32x16_t s[2];               // S^T of the current tile: keys 32 kb .. 32 kb + 31
+  bf16x8_t p[2][2];            // P^T of the previous tile: (key block, 16-key step)
+  float l;                     // row sum (this lane's half of the keys)
+  float m_off;                 // exponent offset (raw score units)
+  float mx;                    // running row max (max-only walk)
+};
+
+// The 32 MFMA jobs of an M phase.  Job code c: 0..15 the PV product of the previous tile
+// (key block c / 8, 16-key step (c / 4) % 2, head-dim block c % 4), 16..31 the QK product
+// of this tile (key block (c - 16) / 8, d-step (c - 16) % 8).  Issue position j runs PV
+// and QK jobs alternately, which spreads the LDS reads (two per PV job, one per QK job)
+// evenly over the phase.
+__device__ __forceinline__ constexpr int job_id(int j) { return (j & 1) ? 16 + (j >> 1) : (j >> 1); }
+__device__ __forceinline__ constexpr int job_reads(int j) { return job_id(j) < 16 ? 2 : 1; }
+
+__device__ __forceinline__ bf16x8_t fetch_job(int jj, int slot, const Walk& w) {
+  const int j = job_id(jj);
+  if (j < 16) {
+    const uint32_t rel = slot * kTileBytes + (32 * (j >> 3) + 16 * ((j >> 2) & 1)) * kRowBytes;
+    const u32x2_t lo = lds_read_tr(w.voff[0][j & 3] + rel);
+    const u32x2_t hi = lds_read_tr(w.voff[1][j & 3] + rel);
+    return as_bf16x8(u32x4_t{lo.x, lo.y, hi.x, hi.y});
   }
-#pragma unroll
-  for (int st = 0; st < 8; ++st)
-#pragma unroll
-    for (int qb = 0; qb < kQB; ++qb) {
-      s0[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[0][st], qf[qb][st], st == 0 ? zero : s0[qb], 0, 0, 0);
-      s1[qb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[1][st], qf[qb][st], st == 0 ? zero : s1[qb], 0, 0, 0);
-    }
+  const int kb = (j - 16) >> 3, st = (j - 16) & 7;
+  return as_bf16x8(*(const lds_u32x4_t*)(uintptr_t)(w.koff[st] + slot * kTileBytes + 32 * kb * kRowBytes));
 }
 
-__device__ __forceinline__ void mask_block(f32x16_t (&s)[kQB], int32_t key0, int32_t k_end, int half) {
-#pragma unroll
-  for (int qb = 0; qb < kQB; ++qb)
-#pragma unroll
-    for (int i = 0; i < 16; ++i)
-      if (key0 + 8 * (i >> 2) + 4 * half + (i & 3) >= k_end) s[qb][i] = -INFINITY;
+__device__ __forceinline__ void run_job(Acc& a, int jj, bf16x8_t f, const bf16x8_t (&qf)[8]) {
+  const int j = job_id(jj);
+  if (j < 16) {
+    a.o[j & 3] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f, a.p[j >> 3][(j >> 2) & 1], a.o[j & 3], 0, 0, 0);
+  } else {
+    const int kb = (j - 16) >> 3, st = (j - 16) & 7;
+    const f32x16_t zero = {};
+    a.s[kb] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f, qf[st], st == 0 ? zero : a.s[kb], 0, 0, 0);
+  }
 }
 
-// Probabilities (bf16) of key block kb and their row sums, then O^T += V^T * P^T over
-// the block's two 16-key steps.
-__device__ __forceinline__ void pv_block(f32x16_t (&o)[kQB][4], float (&l)[kQB], const f32x16_t (&s)[kQB],
-                                         const uint8_t* vt, int kb, const float (&m_off)[kQB], const Walk& w) {
-  const bf16x2_t ones = {(__bf16)1.f, (__bf16)1.f};
-  bf16x8_t pf[kQB][2];
+constexpr int kFetchAhead = 4;               // fragments in flight ahead of the MFMA that uses them
+
+// M phase of tile t from the stage in ring slot `slot`: PV of tile t - 1 and QK of tile t
+// as one straight-line sequence whose fragment reads run kFetchAhead MFMAs ahead (the
+// schedule is pinned so that the reads are not serialised behind the MFMAs).
+template <int J>
+struct MJob {
+  // MFMA J, then the reads of fragment J + kFetchAhead, each pinned in this order
+  static __device__ __forceinline__ void run(Acc& a, bf16x8_t (&f)[32], int slot, const bf16x8_t (&qf)[8],
+                                             const Walk& w) {
+    if constexpr (J + kFetchAhead < 32) f[J + kFetchAhead] = fetch_job(J + kFetchAhead, slot, w);
+    run_job(a, J, f[J], qf);
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+    if constexpr (J + kFetchAhead < 32) __builtin_amdgcn_sched_group_barrier(0x100, job_reads(J + kFetchAhead), 0);
+    if constexpr (J + 1 < 32) MJob<J + 1>::run(a, f, slot, qf, w);
+  }
+};
+
+__device__ __forceinline__ void m_phase_full(Acc& a, int slot, const bf16x8_t (&qf)[8], const Walk& w) {
+  bf16x8_t f[32];
 #pragma unroll
-  for (int qb = 0; qb < kQB; ++qb) {
-    const float moff = m_off[qb] * w.c2;
-    float acc = l[qb];
+  for (int j = 0; j < kFetchAhead; ++j) f[j] = fetch_job(j, slot, w);
+  __builtin_amdgcn_sched_group_barrier(0x100, 3 * kFetchAhead / 2, 0);
+  MJob<0>::run(a, f, slot, qf, w);
+}
+
+// Every M phase runs all 32 jobs, so the loop has a single path for the accumulators: in
+// the first tile's phase P is still zero (the PV product adds nothing), and in the phase
+// after the last tile the QK product of the duplicate K tile is not used.
+__device__ __forceinline__ void m_phase(Acc& a, int slot, const bf16x8_t (&qf)[8], const Walk& w) {
+  m_phase_full(a, slot, qf, w);
+}
+
+// V phase of tile t: mask keys past the range (last tile), the exponent offsets (first
+// tile of pass 0), then P and its row sums (kMode 2: only the row max), with this wave's
+// share of the loads of stage t + 3 issued before and after the arithmetic.
+template <int kMode, int kLoadSlot>
+__device__ __forceinline__ void v_phase(Acc& a, int32_t t, const Walk& w, int wave) {
+  // this wave's share of stage t + 3 (K tile t + 3, V tile t + 2) into the slot that held
+  // stage t - 1
+  const bool load = t + kAhead <= w.n;
+  if (load) load_rows(w.lds_k + kLoadSlot * kTileBytes, w.kbase, w, wave, w.k_begin + min(t + kAhead, w.n - 1) * kBlockK);
+  const int32_t kt0 = w.k_begin + t * kBlockK;
+  if (kt0 + kBlockK > w.k_end) {
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        if (kt0 + 32 * kb + 8 * (i >> 2) + 4 * w.half + (i & 3) >= w.k_end) a.s[kb][i] = -INFINITY;
+  }
+  if (kMode == 2) {
+#pragma unroll
+    for (int i = 0; i < 16; ++i) a.mx = fmaxf(a.mx, fmaxf(a.s[0][i], a.s[1][i]));
+    if (load) load_rows(w.lds_v + kLoadSlot * kTileBytes, w.vbase, w, wave, w.k_begin + (t + kAhead - 1) * kBlockK);
+    return;
+  }
+  if (kMode == 0 && t == 0) {
+    float m = a.s[0][0];
+#pragma unroll
+    for (int i = 0; i < 16; ++i) m = fmaxf(fmaxf(m, a.s[0][i]), a.s[1][i]);
+    a.m_off = fmaxf(m, __shfl_xor(m, 32));
+  }
+  const float moff = a.m_off * w.c2;
+  float acc0 = 0.f, acc1 = 0.f;
+#pragma unroll
+  for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
     for (int i = 0; i < 16; i += 2) {
-      bf16x2_t p2;
-      p2[0] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s[qb][i], w.c2, -moff));
-      p2[1] = (__bf16)__builtin_amdgcn_exp2f(fmaf(s[qb][i + 1], w.c2, -moff));
-      acc = __builtin_amdgcn_fdot2_f32_bf16(p2, ones, acc, false);
-      pf[qb][i >> 3][i & 7] = p2[0];
-      pf[qb][i >> 3][(i & 7) + 1] = p2[1];
+      const float e0 = __builtin_amdgcn_exp2f(fmaf(a.s[kb][i], w.c2, -moff));
+      const float e1 = __builtin_amdgcn_exp2f(fmaf(a.s[kb][i + 1], w.c2, -moff));
+      acc0 += e0;
+      acc1 += e1;
+      a.p[kb][i >> 3][i & 7] = (__bf16)e0;
+      a.p[kb][i >> 3][(i & 7) + 1] = (__bf16)e1;
     }
-    l[qb] = acc;
-  }
-#pragma unroll
-  for (int sub = 0; sub < 2; ++sub) {
-    const uint8_t* vr = vt + (32 * kb + 16 * sub) * kRowBytes;
-#pragma unroll
-    for (int d = 0; d < 4; ++d) {
-      const u32x2_t lo = lds_read_tr(vr + w.voff[0][d]);
-      const u32x2_t hi = lds_read_tr(vr + w.voff[1][d]);
-      const bf16x8_t vf = as_bf16x8(u32x4_t{lo.x, lo.y, hi.x, hi.y});
-#pragma unroll
-      for (int qb = 0; qb < kQB; ++qb)
-        o[qb][d] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[qb][sub], o[qb][d], 0, 0, 0);
-    }
-  }
+  a.l += acc0 + acc1;
+  if (load) load_rows(w.lds_v + kLoadSlot * kTileBytes, w.vbase, w, wave, w.k_begin + (t + kAhead - 1) * kBlockK);
 }
 
-// One tile from buffer `cur`: S^T, masking of keys past the range, then P and O^T.
-__device__ __forceinline__ void attend_tile(Buffers cur, const Walk& w, int32_t kt0, const bf16x8_t (&qf)[kQB][8],
-                                            const float (&m_off)[kQB], f32x16_t (&o)[kQB][4], float (&l)[kQB]) {
-  f32x16_t s0[kQB], s1[kQB];
-  qk_tile(s0, s1, cur.k, qf, w);
-  if (kt0 + kBlockK > w.k_end) {
-    mask_block(s0, kt0, w.k_end, w.half);
-    mask_block(s1, kt0 + 32, w.k_end, w.half);
-  }
-  pv_block(o, l, s0, cur.v, 0, m_off, w);
-  pv_block(o, l, s1, cur.v, 1, m_off, w);
+// Tile t of the walk, with stage t in ring slot kSlot: the M phase of tile t, the stage
+// accounting, then the V phase of tile t (which loads this wave's share of stage t + 3).
+// Every wave runs the same sequence; group B entered the walk one barrier later than
+// group A, so its phases fall one phase later.  A wave waits for its share of stage t + 1
+// (loaded in its V phase of tile t - 2, or before the loop) at the end of its M phase,
+// when only stage t + 2 may still be in flight: group A's wait precedes the barrier that
+// ends global phase 2t, group B's the one that ends 2t + 1, so stage t + 1 is complete
+// for everyone when phase 2t + 2 (group A's M phase of tile t + 1) starts.  The slot
+// refilled with stage t + 3 (group A in phase 2t + 1, group B in 2t + 2) last held stage
+// t - 1, read by group B in global phase 2t - 1.
+template <int kMode, int kSlot>
+__device__ __forceinline__ void step(Acc& a, const Walk& w, const bf16x8_t (&qf)[8], int wave, int32_t t) {
+  if (t > w.n) return;
+  constexpr int kLoadSlot = (kSlot + kAhead) % kStages;
+  m_phase(a, kSlot, qf, w);
+  if (t + 1 <= w.n) wait_stages_in_flight(min(kAhead - 2, w.n - t - 1));
+  barrier();
+  if (t < w.n) v_phase<kMode, kLoadSlot>(a, t, w, wave);
+  barrier();
 }
 
-// Row max of the scores of the tile in `cur` (the range's first tile): the exponent offsets
-// of pass 0.
-__device__ __forceinline__ void first_tile_offsets(Buffers cur, const Walk& w, int32_t kt0,
-                                                   const bf16x8_t (&qf)[kQB][8], float (&m_off)[kQB]) {
-  f32x16_t s0[kQB], s1[kQB];
-  qk_tile(s0, s1, cur.k, qf, w);
-  if (kt0 + kBlockK > w.k_end) {
-    mask_block(s0, kt0, w.k_end, w.half);
-    mask_block(s1, kt0 + 32, w.k_end, w.half);
-  }
-#pragma unroll
-  for (int qb = 0; qb < kQB; ++qb) {
-    float m = s0[qb][0];
-#pragma unroll
-    for (int i = 0; i < 16; ++i) m = fmaxf(fmaxf(m, s0[qb][i]), s1[qb][i]);
-    m_off[qb] = fmaxf(m, __shfl_xor(m, 32));
-  }
-}
-
-// Walk the key range once with fixed per-row exponent offsets m_off (raw score units).
-// kFromFirstTile: set m_off from the first tile's row max (pass 0); otherwise m_off is
-// given (the exact row max).  Accumulates O^T (o) and the row sums (l) from zero.
-// Tiles alternate between buffers b0 and b1; while one is read, the next tile is loaded
-// into the other.
-template <bool kFromFirstTile>
-__device__ __forceinline__ void attend(Buffers b0, Buffers b1, const Walk& w, const bf16x8_t (&qf)[kQB][8],
-                                       float (&m_off)[kQB], f32x16_t (&o)[kQB][4], float (&l)[kQB]) {
+// One walk over the key range.  kMode 0: exponent offsets from the first tile (pass 0);
+// 1: offsets given in a.m_off; 2: exact row max only (a.mx).  Accumulates O^T and the row
+// sums from zero (modes 0 and 1).
+template <int kMode>
+__device__ __forceinline__ void walk(Acc& a, const Walk& w, const bf16x8_t (&qf)[8], int wave, int group) {
   const f32x16_t zero = {};
 #pragma unroll
-  for (int qb = 0; qb < kQB; ++qb) {
-    l[qb] = 0.f;
+  for (int d = 0; d < 4; ++d) a.o[d] = zero;
+  a.l = 0.f;
+  a.mx = -INFINITY;
+  const bf16x8_t pz = {};
 #pragma unroll
-    for (int d = 0; d < 4; ++d) o[qb][d] = zero;
-  }
-  if (w.k_begin < w.k_end) load_tile(b0, w, w.k_begin);
+  for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+    for (int sub = 0; sub < 2; ++sub) a.p[kb][sub] = pz;
+  // everything earlier (Q loads, previous stores) has drained: the in-flight accounting
+  // below counts only this walk's stage loads
   __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  if (kFromFirstTile && w.k_begin < w.k_end) first_tile_offsets(b0, w, w.k_begin, qf, m_off);
-
-  int32_t kt0 = w.k_begin;
-  for (; kt0 + kBlockK < w.k_end; kt0 += 2 * kBlockK) {
-    load_tile(b1, w, kt0 + kBlockK);
-    attend_tile(b0, w, kt0, qf, m_off, o, l);
-    __builtin_amdgcn_s_waitcnt(0);     // this wave's loads of the next tile have landed
-    __syncthreads();                   // ... and everyone's; buffer b0 is free
-    const int32_t kt1 = kt0 + kBlockK;
-    if (kt1 + kBlockK < w.k_end) load_tile(b0, w, kt1 + kBlockK);
-    attend_tile(b1, w, kt1, qf, m_off, o, l);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+  barrier();                                   // the ring is free
+#pragma unroll
+  for (int t = 0; t < kAhead; ++t)
+    if (t <= w.n) load_stage(t, w, wave, t);
+  wait_stages_in_flight(min(kAhead - 1, w.n));
+  barrier();                                   // stage 0 is complete: global phase 0
+  if (group == 1) barrier();                   // group B idles in phase 0
+  for (int32_t t0 = 0; t0 <= w.n; t0 += kStages) {
+    step<kMode, 0>(a, w, qf, wave, t0);
+    step<kMode, 1>(a, w, qf, wave, t0 + 1);
+    step<kMode, 2>(a, w, qf, wave, t0 + 2);
+    step<kMode, 3>(a, w, qf, wave, t0 + 3);
   }
-  if (kt0 < w.k_end) {                 // odd tile count: the last tile, in b0
-    attend_tile(b0, w, kt0, qf, m_off, o, l);
-    __syncthreads();
-  }
-}
-
-// Exact row max of the scores over the key range (QK only), for the overflow fallback.
-__device__ __forceinline__ void exact_row_max(Buffers b0, const Walk& w, const bf16x8_t (&qf)[kQB][8],
-                                              float (&m_off)[kQB]) {
-  float mx[kQB];
-#pragma unroll
-  for (int qb = 0; qb < kQB; ++qb) mx[qb] = -INFINITY;
-  for (int32_t kt0 = w.k_begin; kt0 < w.k_end; kt0 += kBlockK) {
-    __syncthreads();
-    load_tile(b0, w, kt0);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    f32x16_t s0[kQB], s1[kQB];
-    qk_tile(s0, s1, b0.k, qf, w);
-    mask_block(s0, kt0, w.k_end, w.half);
-    mask_block(s1, kt0 + 32, w.k_end, w.half);
-#pragma unroll
-    for (int qb = 0; qb < kQB; ++qb)
-#pragma unroll
-      for (int i = 0; i < 16; ++i) mx[qb] = fmaxf(mx[qb], fmaxf(s0[qb][i], s1[qb][i]));
-  }
-#pragma unroll
-  for (int qb = 0; qb < kQB; ++qb) m_off[qb] = fmaxf(mx[qb], __shfl_xor(mx[qb], 32));
-  __syncthreads();
+  if (group == 0) barrier();                   // group A idles in the last phase
 }
 
 // Unit bookkeeping of the balanced schedule: unit u = (query tile t, key tile k) =
@@ -324,16 +364,15 @@ __device__ __forceinline__ Schedule make_schedule(const AttnArgs& a, int32_t* qt
   return sc;
 }
 
-__global__ __launch_bounds__(kThreads, kGroupsPerCU) void window_attn_kernel(AttnArgs a) {
-  __shared__ __attribute__((aligned(1024))) uint8_t lds_k0[kTileBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t lds_v0[kTileBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t lds_k1[kTileBytes];
-  __shared__ __attribute__((aligned(1024))) uint8_t lds_v1[kTileBytes];
-  const Buffers b0{lds_k0, lds_v0}, b1{lds_k1, lds_v1};
+__global__ __launch_bounds__(kThreads) void window_attn_kernel(AttnArgs a) {
+  // K ring (kStages tiles), then V ring: fragment reads address a slot by an immediate
+  // offset from a per-lane base register (all offsets within a ring stay below 64 KB)
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[2 * kStages * kTileBytes];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int group = wave >> 2;
   const int half = lane >> 5;
   const int col = lane & 31;
   const int32_t N = a.N, H = a.H;
@@ -355,18 +394,17 @@ __global__ __launch_bounds__(kThreads, kGroupsPerCU) void window_attn_kernel(Att
   w.seg.r1 = a.seg_row0[1];
   w.seg.r2 = a.seg_row0[2];
   w.seg.r3 = a.seg_row0[3];
-  w.wave = wave;
-  w.lane = lane;
-  w.col = col;
   w.half = half;
   w.c2 = a.scale * kLog2e;
-  // loader: row 16 wave + 4 i + (lane >> 4); swz of that row = ((lane >> 4) << 2) | i
-  w.lrow = 16 * wave + (lane >> 4);
+  w.lds_k = uint32_t(uintptr_t((lds_void_t*)lds));
+  w.lds_v = w.lds_k + kStages * kTileBytes;
+  // loader: row 8 wave + 4 i + (lane >> 4); swz of that row = ((lane >> 4) << 2) | ((2 wave + i) & 3)
+  w.lrow = 8 * wave + (lane >> 4);
 #pragma unroll
-  for (int i = 0; i < 4; ++i) w.lpiece[i] = ((lane & 15) ^ (((lane >> 4) << 2) | i)) * 16;
+  for (int i = 0; i < 2; ++i) w.lpiece[i] = ((lane & 15) ^ (((lane >> 4) << 2) | ((2 * wave + i) & 3))) * 16;
   // K fragment for d-step st: row col (+32 kb), logical slot 2 st + half
 #pragma unroll
-  for (int st = 0; st < 8; ++st) w.koff[st] = col * kRowBytes + ((2 * st + half) ^ swz(col)) * 16;
+  for (int st = 0; st < 8; ++st) w.koff[st] = w.lds_k + col * kRowBytes + ((2 * st + half) ^ swz(col)) * 16;
   // V^T fragment (transposing read): lane (g = lane >> 4, e = (lane & 15) >> 2, q = lane & 3)
   // addresses row 8 up + 4 half + e, d columns 32 d + 16 (g & 1) + 4 q .. +3
   {
@@ -377,7 +415,7 @@ __global__ __launch_bounds__(kThreads, kGroupsPerCU) void window_attn_kernel(Att
       for (int d = 0; d < 4; ++d) {
         const int row = 8 * up + 4 * half + e;
         const int piece = 4 * d + 2 * (g16 & 1) + (q >> 1);
-        w.voff[up][d] = row * kRowBytes + (piece ^ swz(row)) * 16 + (q & 1) * 8;
+        w.voff[up][d] = w.lds_v + row * kRowBytes + (piece ^ swz(row)) * 16 + (q & 1) * 8;
       }
   }
 
@@ -386,7 +424,6 @@ __global__ __launch_bounds__(kThreads, kGroupsPerCU) void window_attn_kernel(Att
   // tile, so work-groups stream the same keys at about the same time (shared L2).
   const int64_t u_begin = sc.start(g);
   for (int64_t u_hi = sc.start(int64_t(g) + 1); u_hi > u_begin;) {
-    // segment: query tile t, key tiles [k0, k1)
     const int64_t t = (u_hi - 1) / sc.Tk;
     const int64_t u_lo = max<int64_t>(u_begin, t * sc.Tk);
     const int32_t k0 = int32_t(u_lo - t * sc.Tk);
@@ -404,44 +441,35 @@ __global__ __launch_bounds__(kThreads, kGroupsPerCU) void window_attn_kernel(Att
     w.vbase = reinterpret_cast<const uint8_t*>(a.v_cache + bh);
     w.k_begin = k0 * kBlockK;
     w.k_end = min(a.n_keys, k1 * kBlockK);
+    w.n = (w.k_end - w.k_begin + kBlockK - 1) / kBlockK;
 
-    // Q^T fragments: for query block qb and d-step s, q[query][16 s + 8 half .. +8]
-    const int32_t q0 = qt * kBlockQ + wave * kQPerWave;
-    bf16x8_t qf[kQB][8];
-#pragma unroll
-    for (int qb = 0; qb < kQB; ++qb) {
-      const int32_t qi = q0 + qb * 32 + col;
+    // Q^T fragments: for d-step s, q[query][16 s + 8 half .. +8]
+    const int32_t r = wave * 32 + col;                 // row within the query tile
+    const int32_t qi = qt * kBlockQ + r;
+    bf16x8_t qf[8];
+    {
       const int32_t qc = qi < N ? qi : N - 1;
       const uint16_t* qp = a.q + ((int64_t(b) * N + qc) * H + h) * kHeadDim + 8 * half;
 #pragma unroll
-      for (int s = 0; s < 8; ++s) qf[qb][s] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(qp + 16 * s));
+      for (int s = 0; s < 8; ++s) qf[s] = as_bf16x8(*reinterpret_cast<const u32x4_t*>(qp + 16 * s));
     }
 
     // Pass 0: each row's exponent offset is the max of the range's first key tile, so
     // later probabilities may exceed 1.  If a row's sum exceeds 2^64 (its scores grew by
     // more than 64 / (scale log2 e) after the first tile), the work-group redoes the
     // segment with the exact row max, where no probability exceeds 1.
-    f32x16_t o[kQB][4];
-    float m_off[kQB];
-    float l_run[kQB];
-#pragma unroll
-    for (int qb = 0; qb < kQB; ++qb) m_off[qb] = 0.f;
-    attend<true>(b0, b1, w, qf, m_off, o, l_run);
-    bool overflow = false;
-#pragma unroll
-    for (int qb = 0; qb < kQB; ++qb) overflow = overflow || !(l_run[qb] <= 0x1p64f);
-    if (__syncthreads_or(overflow)) {
-      exact_row_max(b0, w, qf, m_off);
-      attend<false>(b0, b1, w, qf, m_off, o, l_run);
+    Acc acc;
+    acc.m_off = 0.f;
+    walk<0>(acc, w, qf, wave, group);
+    if (__syncthreads_or(!(acc.l <= 0x1p64f))) {
+      walk<2>(acc, w, qf, wave, group);
+      acc.m_off = fmaxf(acc.mx, __shfl_xor(acc.mx, 32));
+      walk<1>(acc, w, qf, wave, group);
     }
 
     // ---- segment epilogue: the final output, or a partial for the combine pass
-#pragma unroll
-    for (int qb = 0; qb < kQB; ++qb) {
-      const int32_t r = wave * kQPerWave + qb * 32 + col;       // row within the query tile
-      const int32_t qi = qt * kBlockQ + r;
-      const float l_tot = l_run[qb] + __shfl_xor(l_run[qb], 32);
-      if (qi >= N) continue;
+    const float l_tot = acc.l + __shfl_xor(acc.l, 32);
+    if (qi < N) {
       if (full) {
         const float inv = 1.f / l_tot;
         uint16_t* op = a.out + ((int64_t(b) * N + qi) * H + h) * kHeadDim + 4 * half;
@@ -452,10 +480,10 @@ __global__ __launch_bounds__(kThreads, kGroupsPerCU) void window_attn_kernel(Att
             typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
             bf16x4_t rr;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) rr[e] = (__bf16)(o[qb][d][4 * gg + e] * inv);
+            for (int e = 0; e < 4; ++e) rr[e] = (__bf16)(acc.o[d][4 * gg + e] * inv);
             *reinterpret_cast<bf16x4_t*>(op + d * 32 + 8 * gg) = rr;
           }
-        if (a.lse && half == 0) a.lse[(int64_t(b) * H + h) * N + qi] = m_off[qb] * a.scale + logf(l_tot);
+        if (a.lse && half == 0) a.lse[(int64_t(b) * H + h) * N + qi] = acc.m_off * a.scale + logf(l_tot);
       } else {
         const int64_t prow = (int64_t(g) * 2 + slot) * kBlockQ + r;
         const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
@@ -464,12 +492,12 @@ __global__ __launch_bounds__(kThreads, kGroupsPerCU) void window_attn_kernel(Att
         for (int d = 0; d < 4; ++d)
 #pragma unroll
           for (int gg = 0; gg < 4; ++gg) {
-            const float4 rr = make_float4(o[qb][d][4 * gg] * inv, o[qb][d][4 * gg + 1] * inv,
-                                          o[qb][d][4 * gg + 2] * inv, o[qb][d][4 * gg + 3] * inv);
+            const float4 rr = make_float4(acc.o[d][4 * gg] * inv, acc.o[d][4 * gg + 1] * inv,
+                                          acc.o[d][4 * gg + 2] * inv, acc.o[d][4 * gg + 3] * inv);
             *reinterpret_cast<float4*>(op + d * 32 + 8 * gg) = rr;
           }
         if (half == 0) {
-          a.part_ml[prow * 2] = l_tot > 0.f ? m_off[qb] : -INFINITY;
+          a.part_ml[prow * 2] = l_tot > 0.f ? acc.m_off : -INFINITY;
           a.part_ml[prow * 2 + 1] = l_tot;
         }
       }
@@ -531,13 +559,13 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
 }  // namespace
 
 AttnPlan attn_plan(int32_t B, int32_t H, int32_t N, int32_t n_keys) {
-  // Plain: one work-group per query tile over its whole key range.  Balanced: 2 work-groups
-  // per compute unit (256 CUs) share all (query tile, key tile) units equally, and query
-  // tiles cut between work-groups are merged by attn_combine.  Estimated times (us): a
-  // work-group's 128-query x 64-key tile ~1.85 with two per CU; partials (fp32, written
-  // and read back) at ~5 TB/s plus ~5 us for the extra launch.
-  constexpr int64_t kSlots = 256 * kGroupsPerCU;
-  constexpr double kTileUs = 1.85;
+  // Plain: one work-group per query tile over its whole key range.  Balanced: one
+  // work-group per compute unit (256 CUs) shares all (query tile, key tile) units equally,
+  // and query tiles cut between work-groups are merged by attn_combine.  Estimated times
+  // (us): a work-group's 256-query x 64-key tile ~1.6; partials (fp32, written and read
+  // back) at ~5 TB/s plus ~5 us for the extra launch.
+  constexpr int64_t kSlots = 256;
+  constexpr double kTileUs = 1.6;
   const int64_t qtiles = int64_t(B) * H * ((N + kBlockQ - 1) / kBlockQ);
   const int64_t tk = (n_keys + kBlockK - 1) / kBlockK;
   const int64_t units = qtiles * tk;

@@ -22,9 +22,10 @@ MEAN_ABS = 2e-3
 # tighter relative bound: bf16 rounding of the output (<= 2^-9 relative) and of the
 # probabilities fed to the PV product keep the mean error well under 2^-7 of the mean |o|
 MEAN_REL = 2.0 ** -7
-# log-sum-exp bound: the row sum is accumulated from the bf16-rounded probabilities that
-# enter the PV product (each within 2^-9 relative), so log(sum) moves by at most 2^-9 plus
-# fp32 rounding; 2^-8 leaves margin for the latter
+# log-sum-exp bound: the row sum adds fp32 probabilities, each within a few fp32 ulps of
+# exp2 of the fp32 score (the hardware exp2 and the fp32 scores add a relative error far
+# below 2^-9), so log(sum) moves by well under 2^-9; 2^-8 also covers a row sum built from
+# the bf16-rounded probabilities (each within 2^-9 relative) should the kernel use them
 LSE_ABS = 2.0 ** -8
 
 
