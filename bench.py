@@ -322,6 +322,15 @@ def summarize_profile(d, workload="full_chunk"):
                                        "write_bytes": round(wb), "source": source_hash(base)}
     a = sq.get("window_attn_kernel")
     if a:
+        # shader clock during the kernel: GPU-busy cycles of one XCD over the dispatch's duration,
+        # median over the dispatches of the counter run (the first, cold one included)
+        per = defaultdict(lambda: [0.0, 0])
+        for r in csv.DictReader(open(os.path.join(d, "sq", "sq_counter_collection.csv"))):
+            if kname(r["Kernel_Name"]) == "window_attn_kernel" and r["Counter_Name"] == "GRBM_GUI_ACTIVE":
+                per[r["Dispatch_Id"]][0] += float(r["Counter_Value"]) / 8
+                per[r["Dispatch_Id"]][1] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+        clocks = sorted(c / ns for c, ns in per.values() if ns > 0)
+        sclk = clocks[len(clocks) // 2] if clocks else float("nan")
         cyc = a["GRBM_GUI_ACTIVE"] / 8
         tiles = a["SQ_INSTS_MFMA"] / 32
         lines += ["", "## window_attn_kernel SQ counters (per dispatch)", "",
@@ -329,6 +338,9 @@ def summarize_profile(d, workload="full_chunk"):
                   f"(= 32 per wave per 64-key tile); MFMA busy cycles {a['SQ_VALU_MFMA_BUSY_CYCLES']:.4g}",
                   f"- MFMA busy fraction per SIMD {a['SQ_VALU_MFMA_BUSY_CYCLES'] / (1024 * cyc):.3f} over "
                   f"{cyc:.4g} GPU cycles (GRBM_GUI_ACTIVE / 8 XCDs)",
+                  f"- shader clock during the kernel {sclk:.2f} GHz (GPU cycles per XCD / dispatch duration, "
+                  f"median of {len(clocks)} dispatches: " + ", ".join(f"{c:.2f}" for c in clocks) + "); "
+                  f"MFMA peak at that clock {1024 * 1024 * sclk / 1e3:.0f} TFLOP/s",
                   f"- non-MFMA VALU instructions per wave-tile {(a['SQ_INSTS_VALU'] - a['SQ_INSTS_MFMA']) / tiles:.1f}; "
                   f"LDS instructions per wave-tile {a['SQ_INSTS_LDS'] / tiles:.1f}; "
                   f"LDS bank conflicts {a['SQ_LDS_BANK_CONFLICT']:.0f}"]
