@@ -47,7 +47,8 @@ def parse():
     p.add_argument("--workload", default="full_chunk")
     p.add_argument("--sets", type=int, default=6)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-queries", type=int, default=2048, help="oracle sample: queries x all heads")
+    p.add_argument("--cpu-queries", type=int, default=0,
+                   help="oracle sample: queries x all heads (0 = every query of the chunk, ~4 s on 16 cores)")
     p.add_argument("--summarize-profile", metavar="DIR", default=None,
                    help="read the rocprofv3 CSV output of the profiling commands under DIR (see "
                         "profile_commands()), write profiles/<kernel>_<workload>.md and "
@@ -207,7 +208,7 @@ def cpu_baseline(wl, n_queries):
     nk = (min(wl.S, max(0, wl.f0 - wl.W)) + wl.f0 + wl.C - max(0, wl.f0 - wl.W)) * wl.T
     kc = synth.normal_bf16((wl.B, wl.H, nk, 128), (90, synth.CACHE_K))
     vc = synth.normal_bf16((wl.B, wl.H, nk, 128), (90, synth.CACHE_V))
-    nq = min(n_queries, N)
+    nq = min(n_queries, N) if n_queries > 0 else N
     t0 = time.perf_counter()
     c, s = tables.rope_tables(wl.f0, wl.C, wl.grid_h, wl.grid_w)
     qr = rope.rope_bf16(q, c, s)
