@@ -159,6 +159,26 @@ int unstep_kv_append(unstep_cache* c, int32_t start_frame, int32_t n_frames,
                      const float* cos_t, const float* sin_t,
                      void* q_rot, void* hip_stream);
 
+/* The same pass with the RMS normalisation that precedes RoPE in the paper's model
+ * (Appendix A.6: each query and new key is RMS-normalised over the token's
+ * n_heads*128 channels, then split into heads and rotated).  For every token, separately
+ * for q and k, with C = n_heads*128 and w the per-channel weight:
+ *   ss = sum_i x_i^2                  (fp64; each bf16 square is exact)
+ *   r  = 1 / sqrt(ss / C + norm_eps)  (fp64)
+ *   x'_j = bf16(fp32((x_j * r) * w_j)) (fp64 products, nearest-even roundings)
+ * and x' replaces x in the rotation above; V is stored unchanged.  q_norm_weight,
+ * k_norm_weight: device bf16 [n_heads*128], 16-byte aligned (q_norm_weight is ignored
+ * when q == NULL).  norm_eps: the model's epsilon (1e-6 is the reading taken for the
+ * paper's model; the paper does not state it).  Strides as above.  Errors: those of
+ * unstep_kv_append, plus E_NULL (k_norm_weight; q_norm_weight when q != NULL), E_SHAPE
+ * (n_heads > 32), E_RANGE (norm_eps negative or not finite), E_ALIGN (weights). */
+int unstep_kv_append_qknorm(unstep_cache* c, int32_t start_frame, int32_t n_frames,
+                            const void* q, const void* k, const void* v,
+                            int64_t tok_stride, int64_t head_stride,
+                            const float* cos_t, const float* sin_t,
+                            const void* q_norm_weight, const void* k_norm_weight,
+                            double norm_eps, void* q_rot, void* hip_stream);
+
 /* ---------------------------------------------------------------------------------
  * Windowed block-causal attention (Sections 3.1 and 3.3; Appendix A.3).
  *

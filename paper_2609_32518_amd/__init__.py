@@ -4,7 +4,7 @@ DiT (UnStep, arXiv 2609.32518) on one AMD MI355X.
 Argument marshalling only: every step of the path runs in the library's HIP kernels.
 PyTorch provides device memory (tensors) and the stream; the library's C ABI
 (include/unstep.h) takes raw pointers.  The binding has the same names as the ABI:
-``unstep_rope_tables``, ``unstep_kv_append``, ``unstep_window_attn``, ``unstep_step``
+``unstep_rope_tables``, ``unstep_kv_append`` (+ ``_qknorm``), ``unstep_window_attn``, ``unstep_step``
 as methods/functions below, plus a ``Cache`` handle.
 
 Importing this package loads libunstep.so and raises if it is missing: there is no
@@ -49,6 +49,8 @@ SIGNATURES = {
     "unstep_rope_tables_host": (ctypes.c_int, [_i32, _i32, _i32, _i32, _i32, _f64, _pf32, _pf32]),
     "unstep_rope_tables": (ctypes.c_int, [_i32, _i32, _i32, _i32, _i32, _f64, _vp, _vp, _vp]),
     "unstep_kv_append": (ctypes.c_int, [_vp, _i32, _i32, _vp, _vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp]),
+    "unstep_kv_append_qknorm": (ctypes.c_int, [_vp, _i32, _i32, _vp, _vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp, _f64,
+                                               _vp, _vp]),
     "unstep_attn_workspace_size": (ctypes.c_int, [_vp, _i32, _i32, _i32, ctypes.POINTER(_sz)]),
     "unstep_window_attn": (ctypes.c_int, [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _f32, _vp, _sz, _vp]),
     "unstep_step": (ctypes.c_int, [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp, _vp,
@@ -200,6 +202,27 @@ class Cache:
                                 device=k.device)
         _check(lib.unstep_kv_append(self.handle, start_frame, n_frames, _ptr(q), k.data_ptr(), v.data_ptr(), ts, hs,
                                     cos_t.data_ptr(), sin_t.data_ptr(), _ptr(q_rot), _stream(stream)))
+        return q_rot
+
+    def unstep_kv_append_qknorm(self, start_frame: int, n_frames: int, q: Optional[torch.Tensor], k: torch.Tensor,
+                                v: torch.Tensor, cos_t: torch.Tensor, sin_t: torch.Tensor,
+                                q_norm_weight: Optional[torch.Tensor], k_norm_weight: torch.Tensor,
+                                norm_eps: float = 1e-6, q_rot: Optional[torch.Tensor] = None,
+                                stream=None) -> Optional[torch.Tensor]:
+        """unstep_kv_append with the RMS normalisation of q and k over each token's H*128 channels
+        (weights: bf16 [H*128])."""
+        ts, hs = self._strides(k)
+        if self._strides(v) != (ts, hs) or (q is not None and self._strides(q) != (ts, hs)):
+            raise ValueError("q, k, v must share strides")
+        for w in (k_norm_weight, q_norm_weight):
+            if w is not None and (w.dtype != torch.bfloat16 or w.numel() != self.H * HEAD_DIM or not w.is_contiguous()):
+                raise ValueError("norm weights must be contiguous bf16 [H*128]")
+        if q is not None and q_rot is None:
+            q_rot = torch.empty((self.B, n_frames * self.T, self.H, HEAD_DIM), dtype=torch.bfloat16,
+                                device=k.device)
+        _check(lib.unstep_kv_append_qknorm(self.handle, start_frame, n_frames, _ptr(q), k.data_ptr(), v.data_ptr(),
+                                           ts, hs, cos_t.data_ptr(), sin_t.data_ptr(), _ptr(q_norm_weight),
+                                           k_norm_weight.data_ptr(), norm_eps, _ptr(q_rot), _stream(stream)))
         return q_rot
 
     def unstep_window_attn(self, start_frame: int, n_frames: int, window_frames: int, q_rot: torch.Tensor,

@@ -103,6 +103,9 @@ int plan_append(const unstep_cache* c, const unstep::CacheIndex& idx, int32_t f0
   a.f0 = f0;
   a.S = idx.S();
   a.R = idx.R();
+  a.wq = nullptr;
+  a.wk = nullptr;
+  a.eps = 0.0;
   return UNSTEP_OK;
 }
 
@@ -262,6 +265,34 @@ int unstep_kv_append(unstep_cache* c, int32_t start_frame, int32_t n_frames, con
   if (rc != UNSTEP_OK) return rc;
   hipError_t e = unstep::launch_rope_append(p.args, static_cast<hipStream_t>(hip_stream));
   if (e != hipSuccess) return fail(UNSTEP_E_HIP, "unstep_kv_append: %s", hipGetErrorString(e));
+  c->idx.commit_append(start_frame, n_frames);
+  return ok();
+}
+
+int unstep_kv_append_qknorm(unstep_cache* c, int32_t start_frame, int32_t n_frames, const void* q, const void* k,
+                            const void* v, int64_t tok_stride, int64_t head_stride, const float* cos_t,
+                            const float* sin_t, const void* q_norm_weight, const void* k_norm_weight,
+                            double norm_eps, void* q_rot, void* hip_stream) {
+  const char* where = "unstep_kv_append_qknorm";
+  if (!c) return fail(UNSTEP_E_NULL, "%s: cache handle is NULL", where);
+  if (!k_norm_weight || (q && !q_norm_weight))
+    return fail(UNSTEP_E_NULL, "%s: k_norm_weight (and q_norm_weight when q is given) is NULL", where);
+  if (c->H > unstep::kNormMaxHeads)
+    return fail(UNSTEP_E_SHAPE, "%s: %d heads; the normalising pass handles at most %d", where, c->H,
+                unstep::kNormMaxHeads);
+  if (!(norm_eps >= 0.0) || !std::isfinite(norm_eps))
+    return fail(UNSTEP_E_RANGE, "%s: norm_eps must be finite and >= 0", where);
+  AppendPlan p;
+  int rc = plan_append(c, c->idx, start_frame, n_frames, q, k, v, tok_stride, head_stride, cos_t, sin_t, q_rot,
+                       &p, where);
+  if (rc != UNSTEP_OK) return rc;
+  if (!aligned16(k_norm_weight) || (q && !aligned16(q_norm_weight)))
+    return fail(UNSTEP_E_ALIGN, "%s: norm weights must be 16-byte aligned", where);
+  p.args.wq = q ? static_cast<const uint16_t*>(q_norm_weight) : nullptr;
+  p.args.wk = static_cast<const uint16_t*>(k_norm_weight);
+  p.args.eps = norm_eps;
+  hipError_t e = unstep::launch_rope_append(p.args, static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return fail(UNSTEP_E_HIP, "%s: %s", where, hipGetErrorString(e));
   c->idx.commit_append(start_frame, n_frames);
   return ok();
 }

@@ -27,7 +27,15 @@ struct RopeAppendArgs {
   int32_t B, H, T, C;      // batch, heads, tokens per frame, chunk frames
   int32_t slots;           // cache rows per (batch, head)
   int32_t f0, S, R;        // start frame, sink frames, ring frames
+  // optional RMS normalisation of q and k over each token's H*128 channels before the
+  // rotation: per-channel bf16 weights (wk non-null switches it on; wq non-null iff q is)
+  const uint16_t* wq;
+  const uint16_t* wk;
+  double eps;
 };
+
+// Largest head count of the normalising variant (one wave holds a token's channels).
+constexpr int kNormMaxHeads = 32;
 
 hipError_t launch_rope_append(const RopeAppendArgs& a, hipStream_t stream);
 

@@ -13,7 +13,7 @@ import numpy as np
 import torch
 
 import synth
-from oracle import attention, numerics, rope, tables
+from oracle import attention, numerics, rmsnorm, rope, tables
 from oracle.kvcache import KVCacheOracle
 
 # attention tolerance stated for bf16 inputs with fp32 accumulation
@@ -102,6 +102,28 @@ class Mirror:
         c, s = tables.rope_tables(f0, C, self.gh, self.gw)
         self.orc.append(f0, C, rope.rope_bf16(k, c, s), v)
         return (q, qr, c, s) if with_q else None
+
+    def append_qknorm(self, f0: int, C: int, key, wq_bits, wk_bits, eps=1e-6, with_q=True, q_layout="contiguous",
+                      **kw):
+        """unstep_kv_append_qknorm on both sides; returns (q_rot_dev, q_rot_oracle) (None, None without q)."""
+        q, k, v = self.inputs(C, key, **kw)
+        cos_t, sin_t = self.tables.get(f0, C, self.gh, self.gw)
+        if q_layout == "fused_qkv":
+            qkv = torch.stack([dev(q), dev(k), dev(v)], dim=2)       # [B, N, 3, H, D]
+            qd, kd, vd = qkv[:, :, 0], qkv[:, :, 1], qkv[:, :, 2]
+        else:
+            qd, kd, vd = dev(q), dev(k), dev(v)
+        qr = self.lib.unstep_kv_append_qknorm(f0, C, qd if with_q else None, kd, vd, cos_t, sin_t,
+                                              dev(wq_bits) if with_q else None, dev(wk_bits), eps)
+        c, s = tables.rope_tables(f0, C, self.gh, self.gw)
+        shape = k.shape
+        flat = shape[:-2] + (shape[-2] * shape[-1],)
+        kn = rmsnorm.rms_norm_bf16(k.reshape(flat), wk_bits, eps).reshape(shape)
+        self.orc.append(f0, C, rope.rope_bf16(kn, c, s), v)
+        if not with_q:
+            return None, None
+        qn = rmsnorm.rms_norm_bf16(q.reshape(flat), wq_bits, eps).reshape(shape)
+        return qr, rope.rope_bf16(qn, c, s)
 
     def step(self, f0: int, C: int, W: int, key, use_split=True, lse=False, q_layout="contiguous", **kw):
         """One whole chunk step through unstep_step; returns (q_rot_dev, out_dev, lse_dev, q_rot_oracle)."""

@@ -176,6 +176,28 @@ def test_append_errors_are_caught_before_any_device_work():
     u.lib.unstep_cache_destroy(h)
 
 
+def test_qknorm_append_errors_are_caught_before_any_device_work():
+    rc, h = _handle(1, 2, 2, 3, 0, 4)
+    p = FAKE
+    app = lambda f0=0, C=1, q=None, qr=None, wq=None, wk=p[10], eps=1e-6, k=p[2]: u.lib.unstep_kv_append_qknorm(
+        h, f0, C, q, k, p[3], 256, 128, p[4], p[5], wq, wk, eps, qr, None)
+    assert app(wk=None) == u.E_NULL                                     # k weight required
+    assert app(q=p[6], qr=p[7], wq=None) == u.E_NULL                     # q without its weight
+    assert app(eps=-1.0) == u.E_RANGE
+    assert app(eps=float("inf")) == u.E_RANGE
+    assert app(eps=float("nan")) == u.E_RANGE
+    assert app(wk=p[10] + 8) == u.E_ALIGN
+    assert app(f0=1) == u.E_STATE                                       # the append checks still apply
+    assert app(k=None) == u.E_NULL
+    assert _frame_map(h, 4) == ([-1] * 4, -1)
+    u.lib.unstep_cache_destroy(h)
+    rc, h33 = _handle(1, 33, 2, 3, 0, 4)                                # more heads than one wave holds
+    assert rc == u.OK
+    assert u.lib.unstep_kv_append_qknorm(h33, 0, 1, None, p[2], p[3], 33 * 128, 128, p[4], p[5], None, p[10], 1e-6,
+                                         None, None) == u.E_SHAPE
+    u.lib.unstep_cache_destroy(h33)
+
+
 @pytest.mark.skipif(torch.cuda.is_available(), reason="checks the no-device error path")
 def test_launch_failure_leaves_state_unchanged_without_a_device():
     rc, h = _handle(1, 2, 2, 3, 0, 4)
