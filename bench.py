@@ -47,6 +47,9 @@ def parse():
     p.add_argument("--workload", default="full_chunk")
     p.add_argument("--sets", type=int, default=6)
     p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--qknorm", action="store_true",
+                   help="append with the fused RMS normalisation of q and k (unstep_kv_append_qknorm), "
+                        "then attention, instead of unstep_step")
     p.add_argument("--cpu-queries", type=int, default=0,
                    help="oracle sample: queries x all heads (0 = every query of the chunk, ~4 s on 16 cores)")
     p.add_argument("--summarize-profile", metavar="DIR", default=None,
@@ -71,7 +74,7 @@ def rope_bytes(H, Nq, D=128):
 class Plan:
     """The step's work for one workload: a list of (cache set, start frame, frames, window)."""
 
-    def __init__(self, u, torch, wl, n_sets):
+    def __init__(self, u, torch, wl, n_sets, qknorm=False):
         self.u, self.torch, self.wl = u, torch, wl
         dev = "cuda"
         g = torch.Generator(device=dev)
@@ -80,6 +83,13 @@ class Plan:
         def randn(shape, seed):
             g.manual_seed(seed)
             return torch.randn(shape, generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+
+        self.qknorm = qknorm
+        if qknorm:
+            # learned-norm-like weights around 1
+            g.manual_seed(7)
+            self.wq = (1.0 + 0.1 * torch.randn(wl.H * 128, generator=g, device=dev)).to(torch.bfloat16)
+            self.wk = (1.0 + 0.1 * torch.randn(wl.H * 128, generator=g, device=dev)).to(torch.bfloat16)
 
         self.tables = u.RopeTableCache(dev)
         self.sets = []
@@ -131,8 +141,19 @@ class Plan:
     def per_step(self):
         wl = self.wl
         fl = sum(attn_flops(wl.H, C * wl.T, self.keys(f0, C, W)) * wl.B for (_, f0, C, W) in self.calls)
-        by = sum(rope_bytes(wl.H, C * wl.T) * wl.B for (_, f0, C, W) in self.calls)
+        by = sum(self.append_bytes(C) for (_, f0, C, W) in self.calls)
         return fl, by
+
+    def append_bytes(self, C):
+        wl = self.wl
+        # the normalising pass also reads the two weight vectors (bf16 [H*128]) once
+        return rope_bytes(wl.H, C * wl.T) * wl.B + (4 * wl.H * 128 if self.qknorm else 0)
+
+    def _append(self, s, f0, C, q, k, v, cos_t, sin_t, q_rot):
+        if self.qknorm:
+            s["cache"].unstep_kv_append_qknorm(f0, C, q, k, v, cos_t, sin_t, self.wq, self.wk, q_rot=q_rot)
+        else:
+            s["cache"].unstep_kv_append(f0, C, q, k, v, cos_t, sin_t, q_rot=q_rot)
 
     def _set_for(self, call_set):
         if call_set is not None:
@@ -173,15 +194,18 @@ class Plan:
             q_rot, out = s["q_rot"][:, :N], s["out"][:, :N]
             ws = self.ws.get(si)
             if only == "append":
-                s["cache"].unstep_kv_append(f0, C, q, k, v, cos_t, sin_t, q_rot=q_rot)
+                self._append(s, f0, C, q, k, v, cos_t, sin_t, q_rot)
             elif only == "attn":
                 s["cache"].unstep_window_attn(f0, C, W, q_rot, out=out, workspace=ws)
-            elif events is None:
+            elif events is None and not self.qknorm:
                 s["cache"].unstep_step(f0, C, W, q, k, v, cos_t, sin_t, q_rot=q_rot, out=out, workspace=ws)
+            elif events is None:
+                self._append(s, f0, C, q, k, v, cos_t, sin_t, q_rot)
+                s["cache"].unstep_window_attn(f0, C, W, q_rot, out=out, workspace=ws)
             else:
                 e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
                 e0.record()
-                s["cache"].unstep_kv_append(f0, C, q, k, v, cos_t, sin_t, q_rot=q_rot)
+                self._append(s, f0, C, q, k, v, cos_t, sin_t, q_rot)
                 e1.record()
                 s["cache"].unstep_window_attn(f0, C, W, q_rot, out=out, workspace=ws)
                 e2.record()
@@ -226,6 +250,8 @@ def cpu_baseline(wl, n_queries):
 KERNEL_SOURCES = {
     "window_attn_kernel": ["paper_2609_32518_amd/csrc/window_attn.hip", "paper_2609_32518_amd/csrc/kernels.hpp"],
     "rope_append_kernel": ["paper_2609_32518_amd/csrc/rope_append.hip", "paper_2609_32518_amd/csrc/kernels.hpp"],
+    "rope_norm_append_kernel": ["paper_2609_32518_amd/csrc/rope_append.hip",
+                                "paper_2609_32518_amd/csrc/kernels.hpp"],
 }
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
@@ -249,11 +275,12 @@ def measured_traffic(kernel, workload):
     return rec["bytes_per_launch"]
 
 
-def profile_commands(workload="full_chunk"):
+def profile_commands(workload="full_chunk", qknorm=False):
     """The profiling commands whose output --summarize-profile reads (run from the repo root,
     after `cd /tmp && export TMPDIR=/tmp && cd -`), DIR being their common output folder."""
-    b = f"python -u bench.py --workload {workload} --steps 30 --warmup 30 --no-cpu-baseline"
-    pmc = f"python -u bench.py --workload {workload} --steps 2 --warmup 1 --sets 1 --no-cpu-baseline"
+    q = " --qknorm" if qknorm else ""
+    b = f"python -u bench.py --workload {workload} --steps 30 --warmup 30 --no-cpu-baseline{q}"
+    pmc = f"python -u bench.py --workload {workload} --steps 2 --warmup 1 --sets 1 --no-cpu-baseline{q}"
     cal = "python -u bench.py --copy-calibration 256"
     return [
         ("trace", f"rocprofv3 --kernel-trace --stats -d DIR/trace -o trace --output-format csv -- {b}"),
@@ -266,7 +293,7 @@ def profile_commands(workload="full_chunk"):
     ]
 
 
-def summarize_profile(d, workload="full_chunk"):
+def summarize_profile(d, workload="full_chunk", qknorm=False):
     import csv
     import re
     from collections import defaultdict
@@ -297,10 +324,10 @@ def summarize_profile(d, workload="full_chunk"):
     except (OSError, ValueError):
         traffic = {}
     traffic.setdefault(workload, {})
-    lines = [f"# Kernel profile — {workload} workload", "",
+    lines = [f"# Kernel profile — {workload} workload{' with the RMS-normalising append' if qknorm else ''}", "",
              "Commands (repo root, one MI355X, after `cd /tmp && export TMPDIR=/tmp && cd -`; DIR is an "
              "output folder; this file was written by `python bench.py --summarize-profile DIR`):", "", "```"]
-    lines += [c.replace("DIR", "gpurun_out/prof") for _, c in profile_commands(workload)]
+    lines += [c.replace("DIR", "gpurun_out/prof") for _, c in profile_commands(workload, qknorm)]
     lines += ["```", "", "## Kernel trace (rocprofv3 --kernel-trace --stats)", "",
               "| kernel | calls | average µs | min µs | max µs | % of GPU time |", "|---|---|---|---|---|---|"]
     for r in stats[:6]:
@@ -312,13 +339,13 @@ def summarize_profile(d, workload="full_chunk"):
               "| kernel | FETCH_SIZE KiB | WRITE_SIZE KiB | scaled read MB | scaled write MB | total MB |",
               "|---|---|---|---|---|---|"]
     for k in sorted(set(fetch) | set(write)):
-        if not k.startswith(("window_attn", "attn_combine", "rope_append")):
+        if not k.startswith(("window_attn", "attn_combine", "rope_append", "rope_norm_append")):
             continue
         fk, wk = fetch.get(k, {}).get("FETCH_SIZE", 0.0), write.get(k, {}).get("WRITE_SIZE", 0.0)
         rb, wb = fk * 1024 * f_scale, wk * 1024 * w_scale
         lines.append(f"| {k} | {fk:.0f} | {wk:.0f} | {rb / 1e6:.2f} | {wb / 1e6:.2f} | {(rb + wb) / 1e6:.2f} |")
         base = k.split("<")[0]
-        if base in KERNEL_SOURCES and (base != "rope_append_kernel" or k.endswith("<true>")):
+        if base in KERNEL_SOURCES and (base == "window_attn_kernel" or k.startswith(base + "<true")):
             traffic[workload][base] = {"bytes_per_launch": round(rb + wb), "read_bytes": round(rb),
                                        "write_bytes": round(wb), "source": source_hash(base)}
     a = sq.get("window_attn_kernel")
@@ -345,7 +372,7 @@ def summarize_profile(d, workload="full_chunk"):
                   f"- non-MFMA VALU instructions per wave-tile {(a['SQ_INSTS_VALU'] - a['SQ_INSTS_MFMA']) / tiles:.1f}; "
                   f"LDS instructions per wave-tile {a['SQ_INSTS_LDS'] / tiles:.1f}; "
                   f"LDS bank conflicts {a['SQ_LDS_BANK_CONFLICT']:.0f}"]
-    out = os.path.join(ROOT, "profiles", f"kernels_{workload}.md")
+    out = os.path.join(ROOT, "profiles", f"kernels_{workload}{'_qknorm' if qknorm else ''}.md")
     open(out, "w").write("\n".join(lines) + "\n")
     json.dump(traffic, open(TRAFFIC_FILE, "w"), indent=1, sort_keys=True)
     print("\n".join(lines))
@@ -354,7 +381,7 @@ def summarize_profile(d, workload="full_chunk"):
 def main():
     args = parse()
     if args.summarize_profile:
-        summarize_profile(args.summarize_profile, args.workload)
+        summarize_profile(args.summarize_profile, args.workload, args.qknorm)
         return
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (the step shards by head across GPUs, but no "
@@ -378,7 +405,7 @@ def main():
     import paper_2609_32518_amd as u
 
     wl = synth.WORKLOADS[args.workload]
-    plan = Plan(u, torch, wl, args.sets)
+    plan = Plan(u, torch, wl, args.sets, qknorm=args.qknorm)
     flops, rbytes = plan.per_step()
     torch.cuda.synchronize()
 
@@ -407,7 +434,7 @@ def main():
     else:
         app_ms, att_ms = plan.time_kernels(args.steps)
     per_call_flops = sum(attn_flops(wl.H, C * wl.T, plan.keys(f0, C, W)) * wl.B for (_, f0, C, W) in plan.calls)
-    per_call_bytes = sum(rope_bytes(wl.H, C * wl.T) * wl.B for (_, f0, C, W) in plan.calls)
+    per_call_bytes = sum(plan.append_bytes(C) for (_, f0, C, W) in plan.calls)
     ncalls = len(plan.calls)
     attn_us = att_ms * 1e3 / ncalls
     app_us = app_ms * 1e3 / ncalls
@@ -415,6 +442,7 @@ def main():
     rope_gbs = per_call_bytes / (app_ms * 1e-3) / 1e9
 
     value = flops / (ms * 1e-3) / 1e12
+    app_kernel = "rope_norm_append_kernel" if args.qknorm else "rope_append_kernel"
     res = {
         "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
@@ -423,17 +451,18 @@ def main():
                    "grid": [wl.grid_h, wl.grid_w], "chunk_frames": wl.C, "sink_frames": wl.S,
                    "window_frames": wl.W, "ring_frames": wl.R, "queries": wl.n_query,
                    "keys": plan.keys(wl.f0, wl.C, wl.W), "calls_per_step": len(plan.calls),
-                   "buffer_sets": len(plan.sets), "parallelism": "single GPU"},
+                   "buffer_sets": len(plan.sets), "qk_rmsnorm": bool(args.qknorm), "parallelism": "single GPU"},
         "us_per_step": round(ms * 1e3, 2),
         "host_enqueue_us_per_step": round(t_enq * 1e6 / args.steps, 2),
         "attn": {"kernel": "window_attn", "us_per_call": round(attn_us, 2), "tflops": round(attn_tflops, 2)},
-        "rope_append": {"kernel": "rope_append", "us_per_call": round(app_us, 2), "gbs": round(rope_gbs, 1)},
+        "rope_append": {"kernel": app_kernel[:-len("_kernel")], "us_per_call": round(app_us, 2),
+                        "gbs": round(rope_gbs, 1)},
         "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 2), "peak": PEAK_BF16_TFLOPS,
                      "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
                      "traffic": measured_traffic("window_attn_kernel", wl.name)},
         "rope_roofline": {"bound": "hbm", "achieved": round(rope_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
                           "frac": round(rope_gbs / PEAK_HBM_GBS, 4),
-                          "traffic": measured_traffic("rope_append_kernel", wl.name)},
+                          "traffic": measured_traffic(app_kernel, wl.name)},
     }
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(wl, args.cpu_queries)
