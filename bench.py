@@ -52,6 +52,9 @@ def parse():
                         "then attention, instead of unstep_step")
     p.add_argument("--cpu-queries", type=int, default=0,
                    help="oracle sample: queries x all heads (0 = every query of the chunk, ~4 s on 16 cores)")
+    p.add_argument("--flow-update", action="store_true",
+                   help="only time the clean-cache renoise + emit updates on one chunk's latent "
+                        "(1 x 16 x 3 x 60 x 104 bf16) and print their own JSON line")
     p.add_argument("--summarize-profile", metavar="DIR", default=None,
                    help="read the rocprofv3 CSV output of the profiling commands under DIR (see "
                         "profile_commands()), write profiles/<kernel>_<workload>.md and "
@@ -378,6 +381,43 @@ def summarize_profile(d, workload="full_chunk", qknorm=False):
     print("\n".join(lines))
 
 
+def flow_update_bench(u, torch, args):
+    """Renoise (Equation 1) then emit (Equation 3) at the clean-cache level on a chunk's latent,
+    over rotating buffer sets; per-op time from HIP events around back-to-back launches."""
+    shape = (1, 16, 3, 60, 104)
+    n = math.prod(shape)
+    g = torch.Generator(device="cuda")
+    sets = []
+    for i in range(max(args.sets, 64)):          # ~115 MB: beyond the reuse of one set in L2
+        g.manual_seed(100 + i)
+        mk = lambda: torch.randn(shape, generator=g, device="cuda").to(torch.bfloat16)
+        sets.append((mk(), mk(), mk(), torch.empty(shape, dtype=torch.bfloat16, device="cuda")))
+    sigma = 0.02
+
+    def run(k):
+        x, e, v, o = sets[k % len(sets)]
+        u.unstep_renoise(x, e, sigma, out=o)
+        u.unstep_emit(o, v, sigma, out=o)
+
+    for k in range(args.warmup):
+        run(k)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    e0.record()
+    for k in range(args.steps):
+        run(k)
+    e1.record()
+    torch.cuda.synchronize()
+    us_pair = e0.elapsed_time(e1) * 1e3 / args.steps
+    nbytes = 2 * 3 * 2 * n                       # two ops, each reads two bf16 tensors and writes one
+    print(json.dumps({"metric": "clean-cache renoise + emit µs per chunk latent", "value": round(us_pair, 3),
+                      "unit": "us", "higher_is_better": False, "steps": args.steps, "warmup": args.warmup,
+                      "bytes": nbytes, "gbs": round(nbytes / (us_pair * 1e-6) / 1e9, 1),
+                      "hbm_frac": round(nbytes / (us_pair * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+                      "config": {"latent": list(shape), "sigma": sigma}, "dtype": "bf16 in/out, f64 math",
+                      "data": "synthetic"}), flush=True)
+
+
 def main():
     args = parse()
     if args.summarize_profile:
@@ -404,6 +444,9 @@ def main():
         return
     import paper_2609_32518_amd as u
 
+    if args.flow_update:
+        flow_update_bench(u, torch, args)
+        return
     wl = synth.WORKLOADS[args.workload]
     plan = Plan(u, torch, wl, args.sets, qknorm=args.qknorm)
     flops, rbytes = plan.per_step()

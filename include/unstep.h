@@ -214,6 +214,27 @@ int unstep_step(unstep_cache* c, int32_t start_frame, int32_t n_frames, int32_t 
                 const float* cos_t, const float* sin_t, void* q_rot, void* out, float* lse,
                 float softmax_scale, void* workspace, size_t workspace_bytes, void* hip_stream);
 
+/* ---------------------------------------------------------------------------------
+ * Sampler schedule and clean-cache updates (Section 3.4, Equations 1 and 3, and the
+ * appendix's shift-five schedule; a later row than the attention step).
+ * ------------------------------------------------------------------------------- */
+
+/* Host: the n-step shifted schedule in double precision.  u_i = 1000 (n - i) / n,
+ * sigma_i = shift u_i / (1000 + (shift - 1) u_i), t_i = 1000 sigma_i, for i < n_steps
+ * (the paper's 4 steps with shift 5 give sigma = 1, 15/16, 5/6, 5/8).  sigma_out, t_out:
+ * host double [n_steps].  Errors: E_NULL, E_SHAPE (n_steps < 1), E_RANGE (shift <= 0). */
+int unstep_shift_schedule(int32_t n_steps, double shift, double* sigma_out, double* t_out);
+
+/* Equation 1: x_tilde = (1 - sigma) x + sigma eps on n bf16 values (device, 16-byte
+ * aligned; x_tilde may alias x).  eps is the caller's N(0, I) draw.  Equation 3:
+ * x_next = x_tilde - sigma v.  Arithmetic: each product and the sum/difference in double
+ * precision (no fused multiply-add), then rounded to float and to bf16, both
+ * nearest-even; sigma = 0 makes both identities (the original clean pass), the clean pass
+ * here uses sigma = 0.02.  Errors: E_NULL, E_SHAPE (n < 0), E_RANGE (sigma outside [0, 1]
+ * or NaN), E_ALIGN, E_HIP. */
+int unstep_renoise(const void* x, const void* eps, double sigma, void* x_tilde, int64_t n, void* hip_stream);
+int unstep_emit(const void* x_tilde, const void* v, double sigma, void* x_next, int64_t n, void* hip_stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -52,6 +52,9 @@ SIGNATURES = {
     "unstep_kv_append_qknorm": (ctypes.c_int, [_vp, _i32, _i32, _vp, _vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp, _f64,
                                                _vp, _vp]),
     "unstep_attn_workspace_size": (ctypes.c_int, [_vp, _i32, _i32, _i32, ctypes.POINTER(_sz)]),
+    "unstep_shift_schedule": (ctypes.c_int, [_i32, _f64, ctypes.POINTER(_f64), ctypes.POINTER(_f64)]),
+    "unstep_renoise": (ctypes.c_int, [_vp, _vp, _f64, _vp, _i64, _vp]),
+    "unstep_emit": (ctypes.c_int, [_vp, _vp, _f64, _vp, _i64, _vp]),
     "unstep_window_attn": (ctypes.c_int, [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _f32, _vp, _sz, _vp]),
     "unstep_step": (ctypes.c_int, [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp, _vp,
                                    _f32, _vp, _sz, _vp]),
@@ -263,3 +266,45 @@ class Cache:
 
     def _step_workspace(self, start_frame: int, n_frames: int, window_frames: int) -> Optional[torch.Tensor]:
         return self.workspace(start_frame, n_frames, window_frames)
+
+
+# -- clean-cache updates (Section 3.4) ---------------------------------------------------------
+def unstep_shift_schedule(n_steps: int = 4, shift: float = 5.0):
+    """(sigma, t) float64 numpy arrays of the shifted n-step schedule, built by the library."""
+    import numpy as np
+    sigma = np.zeros(n_steps, np.float64)
+    t = np.zeros(n_steps, np.float64)
+    _check(lib.unstep_shift_schedule(n_steps, shift, sigma.ctypes.data_as(ctypes.POINTER(_f64)),
+                                     t.ctypes.data_as(ctypes.POINTER(_f64))))
+    return sigma, t
+
+
+def _latent(x: torch.Tensor) -> None:
+    if x.dtype != torch.bfloat16 or not x.is_contiguous():
+        raise ValueError("latents must be contiguous bf16 tensors")
+
+
+def unstep_renoise(x: torch.Tensor, eps: torch.Tensor, sigma: float, out: Optional[torch.Tensor] = None,
+                   stream=None) -> torch.Tensor:
+    """Equation 1: (1 - sigma) x + sigma eps."""
+    for t in (x, eps):
+        _latent(t)
+    if eps.shape != x.shape:
+        raise ValueError("x and eps must have the same shape")
+    out = torch.empty_like(x) if out is None else out
+    _latent(out)
+    _check(lib.unstep_renoise(x.data_ptr(), eps.data_ptr(), sigma, out.data_ptr(), x.numel(), _stream(stream)))
+    return out
+
+
+def unstep_emit(x_tilde: torch.Tensor, v: torch.Tensor, sigma: float, out: Optional[torch.Tensor] = None,
+                stream=None) -> torch.Tensor:
+    """Equation 3: x_tilde - sigma v."""
+    for t in (x_tilde, v):
+        _latent(t)
+    if v.shape != x_tilde.shape:
+        raise ValueError("x_tilde and v must have the same shape")
+    out = torch.empty_like(x_tilde) if out is None else out
+    _latent(out)
+    _check(lib.unstep_emit(x_tilde.data_ptr(), v.data_ptr(), sigma, out.data_ptr(), x_tilde.numel(), _stream(stream)))
+    return out

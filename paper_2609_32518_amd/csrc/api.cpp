@@ -347,4 +347,40 @@ int unstep_step(unstep_cache* c, int32_t start_frame, int32_t n_frames, int32_t 
   return ok();
 }
 
+int unstep_shift_schedule(int32_t n_steps, double shift, double* sigma_out, double* t_out) {
+  if (!sigma_out || !t_out) return fail(UNSTEP_E_NULL, "unstep_shift_schedule: output is NULL");
+  if (n_steps < 1) return fail(UNSTEP_E_SHAPE, "unstep_shift_schedule: n_steps must be >= 1");
+  if (!(shift > 0.0) || !std::isfinite(shift)) return fail(UNSTEP_E_RANGE, "unstep_shift_schedule: shift must be > 0");
+  for (int32_t i = 0; i < n_steps; ++i) {
+    const double u = 1000.0 * double(n_steps - i) / double(n_steps);
+    const double sigma = shift * u / (1000.0 + (shift - 1.0) * u);
+    sigma_out[i] = sigma;
+    t_out[i] = 1000.0 * sigma;
+  }
+  return ok();
+}
+
+namespace {
+int flow_update(const char* where, const void* x, const void* y, void* out, int64_t n, double sigma, double a,
+                double b, void* hip_stream) {
+  if (!x || !y || !out) return fail(UNSTEP_E_NULL, "%s: NULL tensor", where);
+  if (n < 0) return fail(UNSTEP_E_SHAPE, "%s: negative element count", where);
+  if (!(sigma >= 0.0 && sigma <= 1.0)) return fail(UNSTEP_E_RANGE, "%s: sigma must lie in [0, 1]", where);
+  if (!aligned16(x) || !aligned16(y) || !aligned16(out)) return fail(UNSTEP_E_ALIGN, "%s: pointers must be 16-byte aligned", where);
+  if (n == 0) return ok();
+  hipError_t e = unstep::launch_flow_update(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(y),
+                                            static_cast<uint16_t*>(out), n, a, b, static_cast<hipStream_t>(hip_stream));
+  if (e != hipSuccess) return fail(UNSTEP_E_HIP, "%s: %s", where, hipGetErrorString(e));
+  return ok();
+}
+}  // namespace
+
+int unstep_renoise(const void* x, const void* eps, double sigma, void* x_tilde, int64_t n, void* hip_stream) {
+  return flow_update("unstep_renoise", x, eps, x_tilde, n, sigma, 1.0 - sigma, sigma, hip_stream);
+}
+
+int unstep_emit(const void* x_tilde, const void* v, double sigma, void* x_next, int64_t n, void* hip_stream) {
+  return flow_update("unstep_emit", x_tilde, v, x_next, n, sigma, 1.0, -sigma, hip_stream);
+}
+
 }  // extern "C"

@@ -66,6 +66,11 @@ struct AttnPlan {
   int32_t plain_groups;    // one work-group per query tile
   size_t part_o_floats;    // offset of the (offset, sum) array in the scratch, in floats
 };
+// out = a x + b y on n bf16 values (renoise / emit of the clean-cache pass); n may be any
+// count, pointers 16-byte aligned.
+hipError_t launch_flow_update(const uint16_t* x, const uint16_t* y, uint16_t* out, int64_t n, double a, double b,
+                              hipStream_t stream);
+
 AttnPlan attn_plan(int32_t B, int32_t H, int32_t N, int32_t n_keys);
 size_t attn_workspace_bytes(int32_t groups);
 hipError_t launch_window_attn(const AttnArgs& a, hipStream_t stream);

@@ -215,3 +215,26 @@ def test_workspace_size_is_shape_only():
     assert u.lib.unstep_attn_workspace_size(h, 0, 1, 11, ctypes.byref(b)) == u.OK
     assert u.lib.unstep_attn_workspace_size(h, 0, 0, 11, ctypes.byref(b)) == u.E_SHAPE
     u.lib.unstep_cache_destroy(h)
+
+
+def test_shift_schedule_bit_identical_to_oracle_and_errors():
+    from oracle import schedule
+    for n, shift in ((4, 5.0), (8, 3.0), (1, 5.0), (6, 1.0)):
+        sigma, t = u.unstep_shift_schedule(n, shift)
+        _, s_ref, t_ref = schedule.shift_schedule(n, shift)
+        assert np.array_equal(sigma, s_ref) and np.array_equal(t, t_ref)
+    d = ctypes.c_double()
+    assert u.lib.unstep_shift_schedule(0, 5.0, ctypes.byref(d), ctypes.byref(d)) == u.E_SHAPE
+    assert u.lib.unstep_shift_schedule(4, 0.0, ctypes.byref(d), ctypes.byref(d)) == u.E_RANGE
+    assert u.lib.unstep_shift_schedule(4, 5.0, None, ctypes.byref(d)) == u.E_NULL
+
+
+def test_renoise_emit_argument_errors():
+    p = FAKE
+    for fn in (u.lib.unstep_renoise, u.lib.unstep_emit):
+        assert fn(None, p[1], 0.02, p[2], 100, None) == u.E_NULL
+        assert fn(p[0], p[1], 0.02, p[2], -1, None) == u.E_SHAPE
+        assert fn(p[0], p[1], 1.5, p[2], 100, None) == u.E_RANGE
+        assert fn(p[0], p[1], float("nan"), p[2], 100, None) == u.E_RANGE
+        assert fn(p[0] + 2, p[1], 0.02, p[2], 100, None) == u.E_ALIGN
+        assert fn(p[0], p[1], 0.02, p[2], 0, None) == u.OK          # nothing to do
