@@ -55,6 +55,17 @@ def parse():
     p.add_argument("--flow-update", action="store_true",
                    help="only time the clean-cache renoise + emit updates on one chunk's latent "
                         "(1 x 16 x 3 x 60 x 104 bf16) and print their own JSON line")
+    p.add_argument("--clip", default=None, choices=["unstep", "unstep_one_step", "self_forcing"],
+                   help="time whole clips instead: the sampler's DiT calls (renoise, one chunk step per "
+                        "attention layer, emit) and print their own JSON line (--clips, --warmup-clips)")
+    p.add_argument("--clip-chunks", type=int, default=7,
+                   help="chunks per clip (7 = the 21 latent frames of an 81-frame, 5 s clip; 41 for 30 s)")
+    p.add_argument("--clips", type=int, default=3, help="timed clips (with --clip)")
+    p.add_argument("--warmup-clips", type=int, default=1)
+    p.add_argument("--layers", type=int, default=30)
+    p.add_argument("--eight-frame-layers", default="odd",
+                   help="layers keeping eight frames (two sinks) instead of nine: 'none', 'all', 'odd', "
+                        "or comma-separated layer indices (the paper does not list them)")
     p.add_argument("--summarize-profile", metavar="DIR", default=None,
                    help="read the rocprofv3 CSV output of the profiling commands under DIR (see "
                         "profile_commands()), write profiles/<kernel>_<workload>.md and "
@@ -418,6 +429,127 @@ def flow_update_bench(u, torch, args):
                       "data": "synthetic"}), flush=True)
 
 
+def clip_bench(u, torch, args):
+    """Whole clips at the paper's shapes: for every DiT call of the sampler, renoise the chunk's
+    latent, run one chunk step (RoPE + KV append + windowed attention) in each of the layers,
+    each layer with its own cache (nine frames: 3 sinks + 6 recent; eight frames: 2 + 6; the
+    original sampler: every frame), then emit.  Synthetic q/k/v, noise and velocities are drawn
+    up front and rotated; the rotary tables of each start frame are built once, on a side stream
+    while the compute stream runs earlier calls, and cached for the process (so the timed clips
+    find them built).  Caches start empty for each clip."""
+    dev = "cuda"
+    H, GH, GW, C = 12, 30, 52, 3
+    T = GH * GW
+    N = C * T
+    L, n_chunks = args.layers, args.clip_chunks
+    if args.eight_frame_layers == "none":
+        eight = set()
+    elif args.eight_frame_layers == "all":
+        eight = set(range(L))
+    elif args.eight_frame_layers == "odd":
+        eight = set(range(1, L, 2))
+    else:
+        eight = {int(x) for x in args.eight_frame_layers.split(",") if x}
+    if args.clip == "self_forcing":
+        windows = [(0, C * n_chunks, C * n_chunks)] * L            # every frame kept
+    else:
+        windows = [((2 if li in eight else 3), C, 2 * C) for li in range(L)]   # (S, W, R)
+    calls = u.unstep_sampler_calls(args.clip, n_chunks)
+    n_calls = len(calls["chunk"])
+
+    g = torch.Generator(device=dev)
+
+    def randn(shape, seed):
+        g.manual_seed(seed)
+        return torch.randn(shape, generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
+
+    pool = [tuple(randn((1, N, H, 128), 50 + 3 * i + j) for j in range(3)) for i in range(8)]   # 345 MB
+    latent = (1, 16, C, 2 * GH, 2 * GW)
+    noise = [randn(latent, 900 + i) for i in range(8)]
+    vel = [randn(latent, 950 + i) for i in range(8)]
+    x = randn(latent, 999)
+    q_rot = torch.empty((1, N, H, 128), dtype=torch.bfloat16, device=dev)
+    out = torch.empty_like(q_rot)
+    bufs = []
+    for (S, W, R) in windows:
+        rows = (S + R) * T
+        bufs.append((torch.zeros((1, H, rows, 128), dtype=torch.bfloat16, device=dev),
+                     torch.zeros((1, H, rows, 128), dtype=torch.bfloat16, device=dev)))
+    side = torch.cuda.Stream()                                     # default priority
+    compute = torch.cuda.current_stream()
+
+    def new_caches():
+        return [u.Cache(1, H, GH, GW, S, R, device=dev, k_cache=k, v_cache=v)
+                for (S, W, R), (k, v) in zip(windows, bufs)]
+
+    # one workspace for every layer and call (the calls run in stream order)
+    probe = new_caches()
+    ws_need = max(probe[li].workspace_bytes(int(f0), C, windows[li][1])
+                  for li in range(L) for f0 in set(calls["start_frame"].tolist()))
+    ws = torch.empty(max(ws_need, 1), dtype=torch.uint8, device=dev)
+    del probe
+
+    flops = 0.0
+    for ci in range(n_calls):
+        f0 = int(calls["start_frame"][ci])
+        for (S, W, R) in windows:
+            lo = max(0, f0 - W)
+            keys = (min(S, lo) + (f0 + C - lo)) * T
+            flops += attn_flops(H, N, keys)
+
+    # rotary tables are cached per start frame for the process (built during the warm-up clip)
+    tables = {}
+
+    def run_clip(xt_buf):
+        caches = new_caches()
+        k = 0
+        for ci in range(n_calls):
+            f0 = int(calls["start_frame"][ci])
+            sigma = float(calls["sigma"][ci])
+            if f0 not in tables:
+                with torch.cuda.stream(side):
+                    tables[f0] = u.unstep_rope_tables(f0, C, GH, GW, stream=side)
+            cos_t, sin_t = tables[f0]
+            u.unstep_renoise(x, noise[ci % 8], sigma, out=xt_buf)
+            for li, cache in enumerate(caches):
+                q, kk, v = pool[k % len(pool)]
+                k += 1
+                cache.unstep_step(f0, C, windows[li][1], q, kk, v, cos_t, sin_t, q_rot=q_rot, out=out,
+                                  workspace=ws)
+            u.unstep_emit(xt_buf, vel[ci % 8], sigma, out=x)
+        return caches
+
+    xt_buf = torch.empty_like(x)
+    for _ in range(max(1, args.warmup_clips)):
+        run_clip(xt_buf)
+    torch.cuda.synchronize()
+    clips = max(1, args.clips)
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    e0.record(compute)
+    for _ in range(clips):
+        run_clip(xt_buf)
+    e1.record(compute)
+    torch.cuda.synchronize()
+    wall = (time.perf_counter() - t0) / clips
+    ms = e0.elapsed_time(e1) / clips
+    latent_frames = C * n_chunks
+    video_frames = 1 + 4 * (latent_frames - 1)
+    tf = flops / (ms * 1e-3) / 1e12
+    print(json.dumps({
+        "metric": "attention path ms per clip (sampler calls x layers: RoPE + KV append + windowed attention, "
+                  "renoise, emit)",
+        "value": round(ms, 3), "unit": "ms", "higher_is_better": False, "clips": clips,
+        "wall_ms_per_clip": round(wall * 1e3, 3), "dit_calls": n_calls, "layer_steps": n_calls * L,
+        "us_per_layer_step": round(ms * 1e3 / (n_calls * L), 2),
+        "attn_tflops": round(tf, 1), "attn_frac_of_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+        "video_frames_per_s_attention_path_only": round(video_frames / (ms * 1e-3), 1),
+        "config": {"workload": f"clip_{args.clip}", "chunks": n_chunks, "latent_frames": latent_frames,
+                   "video_frames": video_frames, "layers": L, "eight_frame_layers": sorted(eight)
+                   if args.clip != "self_forcing" else [], "heads": H, "grid": [GH, GW], "chunk_frames": C},
+        "dtype": "bf16 in, fp32 accumulate", "data": "synthetic"}), flush=True)
+
+
 def main():
     args = parse()
     if args.summarize_profile:
@@ -446,6 +578,9 @@ def main():
 
     if args.flow_update:
         flow_update_bench(u, torch, args)
+        return
+    if args.clip:
+        clip_bench(u, torch, args)
         return
     wl = synth.WORKLOADS[args.workload]
     plan = Plan(u, torch, wl, args.sets, qknorm=args.qknorm)

@@ -235,6 +235,39 @@ int unstep_shift_schedule(int32_t n_steps, double shift, double* sigma_out, doub
 int unstep_renoise(const void* x, const void* eps, double sigma, void* x_tilde, int64_t n, void* hip_stream);
 int unstep_emit(const void* x_tilde, const void* v, double sigma, void* x_next, int64_t n, void* hip_stream);
 
+/* ---------------------------------------------------------------------------------
+ * DiT call sequence of a clip (Section 3.2, Section 3.4 and Appendix A.2).  A clip is
+ * generated in chunks of chunk_frames latent frames; every DiT evaluation of a chunk is one
+ * call at noise level sigma and label t: renoise (Equation 1), the DiT with one
+ * unstep_step per attention layer, emit (Equation 3).  Steps index the four-step
+ * shift-five table (sigma = 1, 15/16, 5/6, 5/8):
+ *   UNSTEP_SAMPLER_SELF_FORCING     every chunk 0, 1, 2, 3
+ *   UNSTEP_SAMPLER_UNSTEP           chunk 0: 0, 1, 2, 3; later chunks 0 then 2 (odd chunks)
+ *                                   or 3 (even chunks), alternating
+ *   UNSTEP_SAMPLER_UNSTEP_ONE_STEP  chunk 0: 0, 1, 2, 3; later chunks 0
+ * and every chunk ends with one clean-cache call, schedule index UNSTEP_SCHEDULE_CLEAN,
+ * t = 0, sigma = clean_sigma (negative selects the variant's own: 0 for Self Forcing, where
+ * renoise and emit are identities, 0.02 for UnStep).
+ * ------------------------------------------------------------------------------- */
+typedef enum {
+  UNSTEP_SAMPLER_SELF_FORCING = 0,
+  UNSTEP_SAMPLER_UNSTEP = 1,
+  UNSTEP_SAMPLER_UNSTEP_ONE_STEP = 2
+} unstep_sampler;
+
+#define UNSTEP_SCHEDULE_CLEAN (-1)
+
+/* Host: writes the calls of a clip of n_chunks chunks in order into the caller's arrays
+ * of `capacity` entries (chunk index, start frame = chunk * chunk_frames, schedule index,
+ * sigma, t) and their count into *n_calls.  *n_calls is set even when the arrays are too
+ * small (then E_RANGE and nothing written), so capacity 0 with NULL arrays asks for the
+ * count.  Errors: E_NULL (n_calls; an array when calls are written), E_SHAPE
+ * (n_chunks < 0, chunk_frames < 1), E_RANGE (unknown variant, clean_sigma above 1 or NaN,
+ * frame indices past int32, capacity below the count). */
+int unstep_sampler_calls(int32_t variant, int32_t n_chunks, int32_t chunk_frames, double clean_sigma,
+                         int32_t capacity, int32_t* n_calls, int32_t* chunk, int32_t* start_frame,
+                         int32_t* schedule_index, double* sigma, double* t_label);
+
 #ifdef __cplusplus
 }
 #endif

@@ -53,6 +53,8 @@ SIGNATURES = {
                                                _vp, _vp]),
     "unstep_attn_workspace_size": (ctypes.c_int, [_vp, _i32, _i32, _i32, ctypes.POINTER(_sz)]),
     "unstep_shift_schedule": (ctypes.c_int, [_i32, _f64, ctypes.POINTER(_f64), ctypes.POINTER(_f64)]),
+    "unstep_sampler_calls": (ctypes.c_int, [_i32, _i32, _i32, _f64, _i32, _pi32, _pi32, _pi32, _pi32,
+                                            ctypes.POINTER(_f64), ctypes.POINTER(_f64)]),
     "unstep_renoise": (ctypes.c_int, [_vp, _vp, _f64, _vp, _i64, _vp]),
     "unstep_emit": (ctypes.c_int, [_vp, _vp, _f64, _vp, _i64, _vp]),
     "unstep_window_attn": (ctypes.c_int, [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _f32, _vp, _sz, _vp]),
@@ -277,6 +279,33 @@ def unstep_shift_schedule(n_steps: int = 4, shift: float = 5.0):
     _check(lib.unstep_shift_schedule(n_steps, shift, sigma.ctypes.data_as(ctypes.POINTER(_f64)),
                                      t.ctypes.data_as(ctypes.POINTER(_f64))))
     return sigma, t
+
+
+SAMPLERS = {"self_forcing": 0, "unstep": 1, "unstep_one_step": 2}
+SCHEDULE_CLEAN = -1
+
+
+def unstep_sampler_calls(variant: str, n_chunks: int, chunk_frames: int = 3, clean_sigma: Optional[float] = None):
+    """The clip's DiT calls from the library: dict of numpy arrays chunk, start_frame,
+    schedule_index (SCHEDULE_CLEAN for the clean-cache call), sigma, t."""
+    import numpy as np
+    if variant not in SAMPLERS:
+        raise ValueError(f"unknown sampler {variant!r}")
+    cs = -1.0 if clean_sigma is None else float(clean_sigma)
+    n = _i32(0)
+    rc = lib.unstep_sampler_calls(SAMPLERS[variant], n_chunks, chunk_frames, cs, 0, ctypes.byref(n), None, None, None,
+                                  None, None)
+    if rc not in (0, -3) or (rc == -3 and n.value == 0):
+        _check(rc)
+    cap = n.value
+    out = dict(chunk=np.zeros(cap, np.int32), start_frame=np.zeros(cap, np.int32),
+               schedule_index=np.zeros(cap, np.int32), sigma=np.zeros(cap, np.float64), t=np.zeros(cap, np.float64))
+    p32 = lambda a: a.ctypes.data_as(_pi32)
+    p64 = lambda a: a.ctypes.data_as(ctypes.POINTER(_f64))
+    _check(lib.unstep_sampler_calls(SAMPLERS[variant], n_chunks, chunk_frames, cs, cap, ctypes.byref(n),
+                                    p32(out["chunk"]), p32(out["start_frame"]), p32(out["schedule_index"]),
+                                    p64(out["sigma"]), p64(out["t"])))
+    return out
 
 
 def _latent(x: torch.Tensor) -> None:

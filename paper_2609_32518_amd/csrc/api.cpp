@@ -360,6 +360,59 @@ int unstep_shift_schedule(int32_t n_steps, double shift, double* sigma_out, doub
   return ok();
 }
 
+int unstep_sampler_calls(int32_t variant, int32_t n_chunks, int32_t chunk_frames, double clean_sigma,
+                         int32_t capacity, int32_t* n_calls, int32_t* chunk, int32_t* start_frame,
+                         int32_t* schedule_index, double* sigma, double* t_label) {
+  if (!n_calls) return fail(UNSTEP_E_NULL, "unstep_sampler_calls: n_calls is NULL");
+  *n_calls = 0;
+  if (variant < UNSTEP_SAMPLER_SELF_FORCING || variant > UNSTEP_SAMPLER_UNSTEP_ONE_STEP)
+    return fail(UNSTEP_E_RANGE, "unstep_sampler_calls: unknown variant %d", variant);
+  if (n_chunks < 0 || chunk_frames < 1)
+    return fail(UNSTEP_E_SHAPE, "unstep_sampler_calls: n_chunks must be >= 0 and chunk_frames >= 1");
+  if (int64_t(n_chunks) * chunk_frames > INT32_MAX)
+    return fail(UNSTEP_E_RANGE, "unstep_sampler_calls: frame indices overflow int32");
+  if (std::isnan(clean_sigma) || clean_sigma > 1.0)
+    return fail(UNSTEP_E_RANGE, "unstep_sampler_calls: clean_sigma must be at most 1 (negative: the default)");
+  const double sc = clean_sigma >= 0.0 ? clean_sigma : variant == UNSTEP_SAMPLER_SELF_FORCING ? 0.0 : 0.02;
+  // steps of chunk c: the four-step table for the first chunk (and every chunk of Self
+  // Forcing); later chunks index 0, then index 2 and 3 alternating (odd chunks 2) for the
+  // two-step variant or nothing more for the one-step variant; then the clean call
+  auto steps = [&](int32_t c, int32_t* idx) -> int {
+    if (c == 0 || variant == UNSTEP_SAMPLER_SELF_FORCING) {
+      for (int i = 0; i < 4; ++i) idx[i] = i;
+      return 4;
+    }
+    idx[0] = 0;
+    if (variant == UNSTEP_SAMPLER_UNSTEP_ONE_STEP) return 1;
+    idx[1] = (c & 1) ? 2 : 3;
+    return 2;
+  };
+  int64_t total = 0;
+  int32_t idx[4];
+  for (int32_t c = 0; c < n_chunks; ++c) total += steps(c, idx) + 1;
+  if (total > INT32_MAX) return fail(UNSTEP_E_RANGE, "unstep_sampler_calls: too many calls");
+  *n_calls = int32_t(total);
+  if (total > capacity)
+    return fail(UNSTEP_E_RANGE, "unstep_sampler_calls: %lld calls do not fit capacity %d", (long long)total, capacity);
+  if (total == 0) return ok();
+  if (!chunk || !start_frame || !schedule_index || !sigma || !t_label)
+    return fail(UNSTEP_E_NULL, "unstep_sampler_calls: output array is NULL");
+  double tab_sigma[4], tab_t[4];
+  unstep_shift_schedule(4, 5.0, tab_sigma, tab_t);
+  int32_t k = 0;
+  for (int32_t c = 0; c < n_chunks; ++c) {
+    const int n = steps(c, idx);
+    for (int i = 0; i <= n; ++i, ++k) {
+      chunk[k] = c;
+      start_frame[k] = c * chunk_frames;
+      schedule_index[k] = i < n ? idx[i] : UNSTEP_SCHEDULE_CLEAN;
+      sigma[k] = i < n ? tab_sigma[idx[i]] : sc;
+      t_label[k] = i < n ? tab_t[idx[i]] : 0.0;
+    }
+  }
+  return ok();
+}
+
 namespace {
 int flow_update(const char* where, const void* x, const void* y, void* out, int64_t n, double sigma, double a,
                 double b, void* hip_stream) {

@@ -238,3 +238,35 @@ def test_renoise_emit_argument_errors():
         assert fn(p[0], p[1], float("nan"), p[2], 100, None) == u.E_RANGE
         assert fn(p[0] + 2, p[1], 0.02, p[2], 100, None) == u.E_ALIGN
         assert fn(p[0], p[1], 0.02, p[2], 0, None) == u.OK          # nothing to do
+
+
+def test_sampler_calls_bit_identical_to_oracle_and_errors():
+    from oracle import sampler
+    for variant in sampler.VARIANTS:
+        for n_chunks in (0, 1, 2, 7, 41):
+            for cs in (None, 0.05):
+                got = u.unstep_sampler_calls(variant, n_chunks, clean_sigma=cs)
+                want = sampler.calls(variant, n_chunks, clean_sigma=cs)
+                assert len(got["chunk"]) == len(want)
+                for key, attr in (("chunk", "chunk"), ("start_frame", "start_frame"), ("schedule_index", "index"),
+                                  ("sigma", "sigma"), ("t", "t")):
+                    assert got[key].tolist() == [getattr(c, attr) for c in want], (variant, n_chunks, key)
+    got = u.unstep_sampler_calls("unstep", 3, chunk_frames=1)
+    assert got["start_frame"].tolist() == [c.start_frame for c in sampler.calls("unstep", 3, chunk_frames=1)]
+    n = ctypes.c_int32(-7)
+    i32 = ctypes.c_int32 * 8
+    f64 = ctypes.c_double * 8
+    a, b, c, d, e = i32(), i32(), i32(), f64(), f64()
+    assert u.lib.unstep_sampler_calls(1, 2, 3, -1.0, 8, None, a, b, c, d, e) == u.E_NULL
+    assert u.lib.unstep_sampler_calls(3, 2, 3, -1.0, 8, ctypes.byref(n), a, b, c, d, e) == u.E_RANGE
+    assert u.lib.unstep_sampler_calls(1, -1, 3, -1.0, 8, ctypes.byref(n), a, b, c, d, e) == u.E_SHAPE
+    assert u.lib.unstep_sampler_calls(1, 2, 0, -1.0, 8, ctypes.byref(n), a, b, c, d, e) == u.E_SHAPE
+    assert u.lib.unstep_sampler_calls(1, 2, 3, 1.5, 8, ctypes.byref(n), a, b, c, d, e) == u.E_RANGE
+    assert u.lib.unstep_sampler_calls(1, 2, 3, float("nan"), 8, ctypes.byref(n), a, b, c, d, e) == u.E_RANGE
+    assert u.lib.unstep_sampler_calls(1, 2**30, 3, -1.0, 8, ctypes.byref(n), a, b, c, d, e) == u.E_RANGE
+    # two chunks of the two-step sampler: 5 + 3 calls; capacity 7 is too small, the count is still reported
+    assert u.lib.unstep_sampler_calls(1, 2, 3, -1.0, 7, ctypes.byref(n), a, b, c, d, e) == u.E_RANGE and n.value == 8
+    assert u.lib.unstep_sampler_calls(1, 2, 3, -1.0, 8, ctypes.byref(n), a, None, c, d, e) == u.E_NULL
+    assert u.lib.unstep_sampler_calls(1, 2, 3, -1.0, 8, ctypes.byref(n), a, b, c, d, e) == u.OK and n.value == 8
+    assert u.lib.unstep_sampler_calls(1, 0, 3, -1.0, 0, ctypes.byref(n), None, None, None, None, None) == u.OK
+    assert n.value == 0
