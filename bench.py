@@ -66,6 +66,9 @@ def parse():
     p.add_argument("--eight-frame-layers", default="odd",
                    help="layers keeping eight frames (two sinks) instead of nine: 'none', 'all', 'odd', "
                         "or comma-separated layer indices (the paper does not list them)")
+    p.add_argument("--summarize-clip-profile", metavar="DIR", default=None,
+                   help="read the kernel trace of a profiled --clip run under DIR and write "
+                        "profiles/kernels_clip_<variant>.md (pass the same --clip arguments)")
     p.add_argument("--summarize-profile", metavar="DIR", default=None,
                    help="read the rocprofv3 CSV output of the profiling commands under DIR (see "
                         "profile_commands()), write profiles/<kernel>_<workload>.md and "
@@ -392,6 +395,71 @@ def summarize_profile(d, workload="full_chunk", qknorm=False):
     print("\n".join(lines))
 
 
+def summarize_clip_profile(d, args):
+    """Per-call breakdown of the last clip in a kernel trace of `bench.py --clip ...`: kernels
+    grouped by the frames each layer attends to (the sampler's call sequence and the layer
+    windows give the order), written to profiles/kernels_clip_<variant>.md."""
+    import csv
+    from collections import defaultdict
+
+    import paper_2609_32518_amd as u
+    variant, L, C, T, H = args.clip, args.layers, 3, 1560, 12
+    calls = u.unstep_sampler_calls(variant, args.clip_chunks)
+    n_calls = len(calls["chunk"])
+    eight = set(range(1, L, 2)) if args.eight_frame_layers == "odd" else \
+        set() if args.eight_frame_layers == "none" else set(range(L)) if args.eight_frame_layers == "all" else \
+        {int(x) for x in args.eight_frame_layers.split(",") if x}
+    sinks = [0 if variant == "self_forcing" else 2 if li in eight else 3 for li in range(L)]
+    window = [C * args.clip_chunks if variant == "self_forcing" else C for _ in range(L)]
+    rows = sorted(csv.DictReader(open(os.path.join(d, "clip_kernel_trace.csv"))), key=lambda r: int(r["Start_Timestamp"]))
+    ours = [r for r in rows if any(k in r["Kernel_Name"] for k in ("rope_append", "window_attn", "attn_combine",
+                                                                       "flow_update"))]
+    fu = [i for i, r in enumerate(ours) if "flow_update" in r["Kernel_Name"]][-2 * n_calls:]
+    groups = defaultdict(list)
+    for c in range(n_calls):
+        f0 = int(calls["start_frame"][c])
+        li = -1
+        for r in ours[fu[2 * c]:fu[2 * c + 1] + 1]:
+            n = r["Kernel_Name"]
+            dur = (int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3
+            if "rope_append" in n:
+                li += 1
+            lo = max(0, f0 - window[max(li, 0)])
+            frames = min(sinks[max(li, 0)], lo) + f0 + C - lo
+            kind = ("rope_append" if "rope_append" in n else "window_attn" if "window_attn" in n else
+                    "attn_combine" if "attn_combine" in n else "flow_update")
+            groups[(kind, frames if kind in ("window_attn", "attn_combine") else 0)].append(dur)
+    span = (int(ours[fu[-1]]["End_Timestamp"]) - int(ours[fu[0]]["Start_Timestamp"])) / 1e3
+    busy = sum(sum(v) for v in groups.values())
+    stats = list(csv.DictReader(open(os.path.join(d, "clip_kernel_stats.csv"))))
+    cmd = (f"rocprofv3 --kernel-trace --stats -d gpurun_out/prof_clip -o clip --output-format csv -- "
+           f"python -u bench.py --clip {variant} --clips 2 --clip-chunks {args.clip_chunks} --layers {L} "
+           f"--eight-frame-layers {args.eight_frame_layers}")
+    lines = [f"# Kernel profile — whole clip, {variant} sampler", "",
+             "Command (repo root, one MI355X, after `cd /tmp && export TMPDIR=/tmp && cd -`); this file was "
+             "written by `python bench.py --summarize-clip-profile gpurun_out/prof_clip` with the same clip "
+             "arguments:", "", "```", cmd, "```", "",
+             f"Clip: {args.clip_chunks} chunks of {C} latent frames, {n_calls} DiT calls x {L} layers, "
+             f"{H} heads x 128, {T} tokens per frame; eight-frame layers: {sorted(eight) if variant != 'self_forcing' else 'none'}.",
+             "", "## Last clip of the trace, by kernel and attended frames", "",
+             f"Span {span / 1e3:.2f} ms; kernels busy {busy / 1e3:.2f} ms ({100 * busy / span:.1f}%).", "",
+             "| kernel | attended frames | launches | average µs | total ms | % of clip | TFLOP/s |",
+             "|---|---|---|---|---|---|---|"]
+    for (kind, fr), v in sorted(groups.items()):
+        avg = sum(v) / len(v)
+        tf = f"{4 * H * C * T * fr * T * 128 / (avg * 1e-6) / 1e12:.0f}" if kind == "window_attn" else ""
+        lines.append(f"| {kind} | {fr or ''} | {len(v)} | {avg:.1f} | {sum(v) / 1e3:.2f} | "
+                     f"{100 * sum(v) / span:.1f} | {tf} |")
+    lines += ["", "## rocprofv3 --stats (whole run: warm-up and timed clips)", "",
+              "| kernel | calls | average µs | % of GPU time |", "|---|---|---|---|"]
+    for r in stats[:8]:
+        lines.append(f"| {r['Name'][:90]} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['Percentage']):.1f} |")
+    out = os.path.join(ROOT, "profiles", f"kernels_clip_{variant}.md")
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def flow_update_bench(u, torch, args):
     """Renoise (Equation 1) then emit (Equation 3) at the clean-cache level on a chunk's latent,
     over rotating buffer sets; per-op time from HIP events around back-to-back launches."""
@@ -554,6 +622,9 @@ def main():
     args = parse()
     if args.summarize_profile:
         summarize_profile(args.summarize_profile, args.workload, args.qknorm)
+        return
+    if args.summarize_clip_profile:
+        summarize_clip_profile(args.summarize_clip_profile, args)
         return
     if args.gpus != 1:
         print(f"bench.py: this build measures one GPU only (the step shards by head across GPUs, but no "
