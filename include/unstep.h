@@ -3,7 +3,7 @@
  * (UnStep, arXiv 2609.32518), for one AMD MI355X (gfx950).
  *
  * One self-attention step for a chunk of C latent frames (Section 3.1, Section 3.3,
- * Appendix A.3 and A.6 of the paper):
+ * Appendix A.3 and A.5 of the paper):
  *   1. rotate the chunk's queries and keys with cached fp32 cos/sin tables (3D RoPE);
  *   2. write the rotated keys and the values into a sink + ring-buffer KV cache whose
  *      positions are held on the host;
@@ -26,7 +26,7 @@
  *     unstep_last_error() then describes the failure.  All argument and state checks
  *     happen before any work is enqueued; a failed call changes no state.
  *   - A cache handle is not thread-safe; distinct handles are independent.
- *   - Only head_dim == 128 is supported (the model's 12 heads of width 128, App. A.6).
+ *   - Only head_dim == 128 is supported (the model's 12 heads of width 128, App. A.5).
  */
 #ifndef UNSTEP_H
 #define UNSTEP_H
@@ -59,7 +59,7 @@ int unstep_version(void);
 const char* unstep_last_error(void);
 
 /* ---------------------------------------------------------------------------------
- * KV cache handle: host-held positions (Section 3.1 and Appendix A.6: the positions
+ * KV cache handle: host-held positions (Section 3.1 and Appendix A.5: the positions
  * depend only on token counts, so they live on the CPU and no call reads the GPU).
  *
  * Slots: S sink slots hold frames 0..S-1; R ring slots hold every later frame f at
@@ -107,7 +107,7 @@ int unstep_window_segments(const unstep_cache* c, int32_t start_frame, int32_t n
                            int32_t* n_seg);
 
 /* ---------------------------------------------------------------------------------
- * Rotary tables (Appendix A.6: fp32 cos/sin per token and coordinate pair, shared by
+ * Rotary tables (Appendix A.5: fp32 cos/sin per token and coordinate pair, shared by
  * all heads, cached per (start latent frame, grid size)).
  *
  * Pair j = 0..head_dim/2-1 belongs to the temporal axis for j < d_t/2, to the grid
@@ -133,7 +133,7 @@ int unstep_rope_tables(int32_t start_frame, int32_t n_frames, int32_t grid_h, in
                        void* hip_stream);
 
 /* ---------------------------------------------------------------------------------
- * Fused RoPE + KV append (Section 3.1 and Appendix A.6; one bandwidth-bound pass).
+ * Fused RoPE + KV append (Section 3.1 and Appendix A.5; one bandwidth-bound pass).
  *
  * For every chunk token n, head h, pair j (x_e = x[2j], x_o = x[2j+1], c/s the table
  * entries of token n, pair j):  y_e = x_e*c - x_o*s,  y_o = x_e*s + x_o*c, each
@@ -148,7 +148,7 @@ int unstep_rope_tables(int32_t start_frame, int32_t n_frames, int32_t grid_h, in
  *
  * Index update (host): the chunk may start at most one frame after the newest stored
  * frame; re-appending stored frames overwrites them in place without advancing the
- * positions (repeated denoising calls, App. A.6); new frames evict the ring slot's
+ * positions (repeated denoising calls, App. A.5); new frames evict the ring slot's
  * previous frame.  Errors: E_NULL (c, k, v, cos_t, sin_t; q_rot when q != NULL),
  * E_SHAPE (n_frames < 1, strides too small), E_ALIGN, E_RANGE (start_frame < 0; more
  * ring frames than the ring holds), E_STATE (gap after the newest frame; a re-appended
@@ -160,7 +160,7 @@ int unstep_kv_append(unstep_cache* c, int32_t start_frame, int32_t n_frames,
                      void* q_rot, void* hip_stream);
 
 /* The same pass with the RMS normalisation that precedes RoPE in the paper's model
- * (Appendix A.6: each query and new key is RMS-normalised over the token's
+ * (Appendix A.5: each query and new key is RMS-normalised over the token's
  * n_heads*128 channels, then split into heads and rotated).  For every token, separately
  * for q and k, with C = n_heads*128 and w the per-channel weight:
  *   ss = sum_i x_i^2                  (fp64; each bf16 square is exact)

@@ -7,12 +7,12 @@ it (only the seeded input generators in ``synth`` serve both).
 
 What it defines, each in fp64 unless the paper fixes a precision:
 
-* ``tables``   -- the per-chunk rotary cos/sin tables (Appendix A.6: cached fp32
+* ``tables``   -- the per-chunk rotary cos/sin tables (Appendix A.5: cached fp32
                   coefficients keyed by start frame and grid).
-* ``rope``     -- the pair rotation of Appendix A.6 under the rounding contract
+* ``rope``     -- the pair rotation of Appendix A.5 under the rounding contract
                   "bf16 in, fp32 math, bf16 out", plus the ideal fp64 rotation.
 * ``kvcache``  -- the sink + sliding-window KV cache with host-held indices
-                  (Section 3.1, Section 3.3, Appendix A.3, Appendix A.6).
+                  (Section 3.1, Section 3.3, Appendix A.3, Appendix A.5).
 * ``attention`` -- exact softmax attention of the chunk's queries over the
                   retained keys, and a brute-force full-timeline masked version.
 

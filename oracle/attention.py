@@ -1,5 +1,5 @@
 """Softmax attention of a chunk's queries over its retained keys (paper Sections 3.1
-and 3.3; Appendix A.3 and A.6).
+and 3.3; Appendix A.3 and A.5).
 
 The windowed step is exact attention over a smaller key set, so the oracle is
 the definition written out in float64:

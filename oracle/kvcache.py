@@ -1,5 +1,5 @@
 """Sink + sliding-window KV cache with host-held indices (paper Sections 3.1, 3.3;
-Appendix A.3 and A.6).
+Appendix A.3 and A.5).
 
 The paper keeps the first latent frames as attention sinks and a window of the
 most recent frames, evicting the middle; the cache positions are host integers

@@ -1,4 +1,4 @@
-"""RMS normalisation of a token's query or key vector before RoPE (Appendix A.6 of the paper).
+"""RMS normalisation of a token's query or key vector before RoPE (Appendix A.5 of the paper).
 
 The paper's model reshapes each query and newly computed key into heads *after* the
 linear projection and an RMS normalisation, so the normalisation runs over all H*D

@@ -1,4 +1,4 @@
-"""Rotary embedding of query/key vectors (Section 3.1 and Appendix A.6 of the paper).
+"""Rotary embedding of query/key vectors (Section 3.1 and Appendix A.5 of the paper).
 
 For one token and one head, pair j = 0..D/2-1 is (x[2j], x[2j+1]) (interleaved
 pairs).  With that token's cached coefficients c = cos, s = sin for pair j:

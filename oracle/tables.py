@@ -1,4 +1,4 @@
-"""Per-chunk 3D rotary cos/sin tables (Appendix A.6 of the paper).
+"""Per-chunk 3D rotary cos/sin tables (Appendix A.5 of the paper).
 
 The paper builds, once per (start latent frame, grid size), fp32 cos and sin
 tables holding one coefficient per token and coordinate pair, shared by all

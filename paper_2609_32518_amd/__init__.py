@@ -116,7 +116,7 @@ def unstep_rope_tables(start_frame: int, n_frames: int, grid_h: int, grid_w: int
 
 class RopeTableCache:
     """Tables keyed by (start frame, n_frames, grid_h, grid_w, theta), built once and reused
-    by every layer and denoising call of that chunk (Appendix A.6)."""
+    by every layer and denoising call of that chunk (Appendix A.5)."""
 
     def __init__(self, device="cuda"):
         self.device = device

@@ -1,5 +1,5 @@
 // Host-held positions of the sink + ring KV cache (paper Section 3.1, Section 3.3,
-// Appendix A.3 and A.6).  Pure C++: no HIP calls, so it is exercised on machines
+// Appendix A.3 and A.5).  Pure C++: no HIP calls, so it is exercised on machines
 // without a GPU.
 //
 // Frames f < S live in sink slot f; later frames in ring slot S + (f - S) mod R.

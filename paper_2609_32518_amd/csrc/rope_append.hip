@@ -1,5 +1,5 @@
 // Fused rotary embedding of the chunk's queries and keys plus the K/V cache write
-// (paper Section 3.1 and Appendix A.6): one bandwidth-bound pass over q, k, v.
+// (paper Section 3.1 and Appendix A.5): one bandwidth-bound pass over q, k, v.
 //
 // Each thread owns 16 bytes (8 bf16 = 4 coordinate pairs) of one (token, head) row of
 // q, k and v.  It loads them with the token's cos/sin for those 4 pairs, rotates q and
@@ -86,7 +86,7 @@ __global__ __launch_bounds__(kThreads) void rope_append_kernel(RopeAppendArgs a)
   }
 }
 
-// ---- variant with RMS normalisation of q and k (Appendix A.6: the model normalises each
+// ---- variant with RMS normalisation of q and k (Appendix A.5: the model normalises each
 // query and new key over the token's H*128 channels, with learned per-channel weights,
 // before splitting it into heads and rotating).
 //

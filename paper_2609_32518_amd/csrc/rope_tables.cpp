@@ -1,4 +1,4 @@
-// Per-chunk rotary cos/sin tables, built on the host (paper Appendix A.6: fp32
+// Per-chunk rotary cos/sin tables, built on the host (paper Appendix A.5: fp32
 // coefficients per token and coordinate pair, shared by all heads, cached per start
 // latent frame and grid size and reused by every layer and denoising call).
 //

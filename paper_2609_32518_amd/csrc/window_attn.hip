@@ -507,21 +507,23 @@ __global__ __launch_bounds__(kThreads) void window_attn_kernel(AttnArgs a) {
 
 // Finish every query tile whose key range was shared by several work-groups: merge their
 // partials by log-sum-exp, out = sum_p w_p o_p / sum_p w_p with w_p = l_p 2^((m_p - M) c2),
-// M = max_p m_p.  Thread = (query tile, row, 4 output columns).
+// M = max_p m_p.  Work-group = (query tile, 8 rows), thread = (row, 4 output columns), so the
+// schedule arithmetic (64-bit divisions) is work-group uniform and runs once per wave on the
+// scalar unit, and each wave reads two whole 512-byte partial rows per load instruction.
+constexpr int kCombineRows = 8;
+
 __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
   int32_t qtiles;
   const Schedule sc = make_schedule(a, &qtiles);
-  const int64_t idx = int64_t(blockIdx.x) * 256 + threadIdx.x;
-  const int64_t t = idx / (kBlockQ * (kHeadDim / 4));
-  if (t >= int64_t(a.B) * a.H * qtiles) return;
-  const int32_t r = int32_t((idx / (kHeadDim / 4)) % kBlockQ);
-  const int32_t part = int32_t(idx % (kHeadDim / 4));
+  constexpr int kGroupsPerTile = kBlockQ / kCombineRows;
+  const int64_t t = blockIdx.x / kGroupsPerTile;                       // (b, h, query tile)
   const int32_t qt = int32_t(t % qtiles);
+  const int32_t r = int32_t(blockIdx.x % kGroupsPerTile) * kCombineRows + int32_t(threadIdx.x >> 5);
+  const int32_t part = threadIdx.x & 31;
   const int32_t qi = qt * kBlockQ + r;
-  if (qi >= a.N) return;
   const int64_t ua = t * sc.Tk;
   const int64_t ga = sc.owner(ua), gb = sc.owner(ua + sc.Tk - 1);
-  if (ga == gb) return;                               // written directly by its work-group
+  if (ga == gb || qi >= a.N) return;                                  // written directly by its work-group
   const float c2 = a.scale * kLog2e;
   float M = -INFINITY;
   for (int64_t g = ga; g <= gb; ++g) {
@@ -589,8 +591,7 @@ hipError_t launch_window_attn(const AttnArgs& a, hipStream_t stream) {
   hipError_t e = hipGetLastError();
   if (e != hipSuccess || a.part_o == nullptr) return e;
   const int64_t qtiles = int64_t(a.B) * a.H * ((a.N + kBlockQ - 1) / kBlockQ);
-  const int64_t work = qtiles * kBlockQ * (kHeadDim / 4);
-  hipLaunchKernelGGL(attn_combine_kernel, dim3(unsigned((work + 255) / 256)), dim3(256), 0, stream, a);
+  hipLaunchKernelGGL(attn_combine_kernel, dim3(unsigned(qtiles * (kBlockQ / kCombineRows))), dim3(256), 0, stream, a);
   return hipGetLastError();
 }
 

@@ -6,7 +6,7 @@ mapping, no attention.  It only
 
 * names the workloads (shapes of the causal video DiT's self-attention step:
   12 heads of width 128, 30x52 = 1560 tokens per latent frame, 3-frame chunks;
-  the paper's Appendix A.1 and A.6 fix these), and
+  the paper's Appendix A.1 and A.5 fix these), and
 * draws seeded N(0,1) values and rounds them to bfloat16 bit patterns.
 
 Every random draw comes from NumPy's PCG64 seeded by a SeedSequence whose key

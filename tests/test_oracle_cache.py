@@ -1,4 +1,4 @@
-"""Pins for the oracle's sink + window KV cache (paper Sections 3.1, 3.3; Appendix A.3, A.6).
+"""Pins for the oracle's sink + window KV cache (paper Sections 3.1, 3.3; Appendix A.3, A.5).
 
 * closed forms the paper states: 1560 tokens per frame, 32760 keys for the full
   21-frame context, 14040 keys for 3 sinks + 6 recent frames;

@@ -1,4 +1,4 @@
-"""Pins for the oracle's rotary embedding (paper Appendix A.6 pair arithmetic).
+"""Pins for the oracle's rotary embedding (paper Appendix A.5 pair arithmetic).
 
 * the rotation equals the complex product (x_2j + i x_2j+1) * exp(i angle),
   the form the paper gives for the original fp64 path;

@@ -94,3 +94,9 @@ def test_layer_windows_match_the_budget(budget):
 def test_unknown_variant():
     with pytest.raises(ValueError):
         sampler.calls("nope", 2)
+
+
+def test_dit_forwards_of_the_five_second_clip():
+    g = GOLDEN["dit_forwards_per_clip"]
+    assert len(sampler.calls("self_forcing", g["chunks"])) == g["self_forcing"]
+    assert len(sampler.calls("unstep", g["chunks"])) == g["unstep"]

@@ -1,4 +1,4 @@
-"""Pins for the oracle's rotary tables (paper Appendix A.6).
+"""Pins for the oracle's rotary tables (paper Appendix A.5).
 
 Each test checks the oracle against something other than itself: the paper's
 worked positions, textbook values of cos/sin, closed forms of the frequency
