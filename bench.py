@@ -55,6 +55,9 @@ def parse():
     p.add_argument("--flow-update", action="store_true",
                    help="only time the clean-cache renoise + emit updates on one chunk's latent "
                         "(1 x 16 x 3 x 60 x 104 bf16) and print their own JSON line")
+    p.add_argument("--oproj", action="store_true",
+                   help="time the projection after attention (y = x W^T + b, 4680 x 1536 x 1536 bf16) and "
+                        "the init-time V/O truncated SVD of one 1536 x 1536 weight; print their own JSON line")
     p.add_argument("--clip", default=None, choices=["unstep", "unstep_one_step", "self_forcing"],
                    help="time whole clips instead: the sampler's DiT calls (renoise, one chunk step per "
                         "attention layer, emit) and print their own JSON line (--clips, --warmup-clips)")
@@ -466,6 +469,48 @@ def summarize_clip_profile(d, args):
     print("\n".join(lines))
 
 
+def oproj_bench(u, torch, args):
+    """The output projection of the full-frame chunk's attention output ([4680, 12 x 128] x
+    [1536, 1536]^T + bias, bf16) over rotating inputs, HIP events around back-to-back calls;
+    then the V/O truncated SVD of one 1536 x 1536 float32 weight at rank 1413 (init time)."""
+    dev = "cuda"
+    M, N, K = 4680, 1536, 1536
+    g = torch.Generator(device=dev)
+    g.manual_seed(11)
+    xs = [torch.randn((M, K), generator=g, device=dev).to(torch.bfloat16) for _ in range(16)]   # 230 MB
+    w32 = torch.randn((N, K), generator=g, device=dev) / math.sqrt(K)
+    b = torch.randn((N,), generator=g, device=dev).to(torch.bfloat16)
+    r = u.vo_rank(K)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    _, w, _ = u.unstep_svd_truncate(w32, r)
+    svd_ms = (time.perf_counter() - t0) * 1e3
+    t0 = time.perf_counter()
+    u.unstep_svd_truncate(w32, r)
+    svd_ms2 = (time.perf_counter() - t0) * 1e3
+    y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
+    for k in range(max(args.warmup, 20)):
+        u.unstep_linear(xs[k % 16], w, b, out=y)
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    n = max(args.steps, 100)
+    e0.record()
+    for k in range(n):
+        u.unstep_linear(xs[k % 16], w, b, out=y)
+    e1.record()
+    torch.cuda.synchronize()
+    us = e0.elapsed_time(e1) * 1e3 / n
+    flops = 2.0 * M * N * K
+    tf = flops / (us * 1e-6) / 1e12
+    print(json.dumps({"metric": "output projection µs per chunk (4680 x 1536 x 1536 bf16 + bias)",
+                      "value": round(us, 2), "unit": "us", "higher_is_better": False, "calls": n,
+                      "tflops": round(tf, 1), "frac_of_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
+                      "svd_truncate_ms": {"first_call": round(svd_ms, 1), "second_call": round(svd_ms2, 1),
+                                          "shape": [N, K], "rank": r},
+                      "config": {"M": M, "N": N, "K": K, "bias": True}, "dtype": "bf16, fp32 accumulate",
+                      "data": "synthetic"}), flush=True)
+
+
 def flow_update_bench(u, torch, args):
     """Renoise (Equation 1) then emit (Equation 3) at the clean-cache level on a chunk's latent,
     over rotating buffer sets; per-op time from HIP events around back-to-back launches."""
@@ -658,6 +703,9 @@ def main():
         return
     if args.clip:
         clip_bench(u, torch, args)
+        return
+    if args.oproj:
+        oproj_bench(u, torch, args)
         return
     wl = synth.WORKLOADS[args.workload]
     plan = Plan(u, torch, wl, args.sets, qknorm=args.qknorm)

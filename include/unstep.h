@@ -268,6 +268,36 @@ int unstep_sampler_calls(int32_t variant, int32_t n_chunks, int32_t chunk_frames
                          int32_t capacity, int32_t* n_calls, int32_t* chunk, int32_t* start_frame,
                          int32_t* schedule_index, double* sigma, double* t_label);
 
+/* ---------------------------------------------------------------------------------
+ * V/O truncated SVD and the projection after attention (Section 3.5 and Appendix A.4:
+ * the value and output weights of layers 8-29 are replaced, once at initialisation, by
+ * their rank r = round(0.92 * 1536) = 1413 reconstruction W_r = U_r S_r V_r^T, kept dense
+ * in W's shape, so the projection's cost is unchanged).
+ * ------------------------------------------------------------------------------- */
+
+/* Init-time: W_r of w (device float32, row-major [rows, cols]) at the given rank, computed
+ * in float64 (the leading singular subspace from rocSOLVER's eigendecomposition of the
+ * smaller Gram matrix, W_r = W V_r V_r^T, with rocBLAS GEMMs; the paper uses float32, whose
+ * rocSOLVER SVD is far less accurate than float32 rounding) and written,
+ * rounded to nearest even, to w_r (device float32 [rows, cols]) and/or w_r_bf16 (device
+ * bf16, the float32 value rounded again: the paper's cast of the float32 weights); sigma_out (optional host float [min(rows, cols)]) receives the singular
+ * values in decreasing order.  w is not modified; w_r may alias w.  Allocates scratch device
+ * memory and returns after the work on hip_stream finished.  Errors: E_NULL (w, or both
+ * outputs), E_SHAPE (rows or cols < 1, more than 2^28 values), E_RANGE (rank outside
+ * [0, min(rows, cols)]), E_ALIGN, E_HIP (including an SVD that did not converge). */
+int unstep_svd_truncate(const float* w, int32_t rows, int32_t cols, int32_t rank, float* w_r, void* w_r_bf16,
+                        float* sigma_out, void* hip_stream);
+
+/* y = x W^T + b: x bf16 [M, K] (e.g. the attention output [tokens, heads * 128]), w bf16
+ * [N, K] (the nn.Linear layout [out, in]), bias bf16 [N] or NULL, y bf16 [M, N]; all
+ * row-major and contiguous, on the device.  float32 accumulation and bias add, bf16 result
+ * (a plain GEMM with a bias epilogue, run by hipBLASLt on hip_stream).  The first call on a
+ * device creates the GEMM library's handle; each new shape picks its algorithm once.
+ * Errors: E_NULL (x, w, y), E_SHAPE (sizes < 1, K or N not a multiple of 8, no algorithm for
+ * the shape), E_ALIGN, E_HIP. */
+int unstep_linear(const void* x, const void* w, const void* bias, void* y, int32_t M, int32_t N, int32_t K,
+                  void* hip_stream);
+
 #ifdef __cplusplus
 }
 #endif

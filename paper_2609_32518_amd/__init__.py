@@ -53,6 +53,8 @@ SIGNATURES = {
                                                _vp, _vp]),
     "unstep_attn_workspace_size": (ctypes.c_int, [_vp, _i32, _i32, _i32, ctypes.POINTER(_sz)]),
     "unstep_shift_schedule": (ctypes.c_int, [_i32, _f64, ctypes.POINTER(_f64), ctypes.POINTER(_f64)]),
+    "unstep_svd_truncate": (ctypes.c_int, [_vp, _i32, _i32, _i32, _vp, _vp, ctypes.POINTER(_f32), _vp]),
+    "unstep_linear": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _vp]),
     "unstep_sampler_calls": (ctypes.c_int, [_i32, _i32, _i32, _f64, _i32, _pi32, _pi32, _pi32, _pi32,
                                             ctypes.POINTER(_f64), ctypes.POINTER(_f64)]),
     "unstep_renoise": (ctypes.c_int, [_vp, _vp, _f64, _vp, _i64, _vp]),
@@ -279,6 +281,44 @@ def unstep_shift_schedule(n_steps: int = 4, shift: float = 5.0):
     _check(lib.unstep_shift_schedule(n_steps, shift, sigma.ctypes.data_as(ctypes.POINTER(_f64)),
                                      t.ctypes.data_as(ctypes.POINTER(_f64))))
     return sigma, t
+
+
+# -- V/O truncated SVD and the projection after attention (Section 3.5, Appendix A.4) -------------
+def vo_rank(m: int, retain: float = 0.92) -> int:
+    """r = round(retain * m): 1413 for the model's 1536-wide projections."""
+    import math
+    return int(math.floor(retain * m + 0.5))
+
+
+def unstep_svd_truncate(w: torch.Tensor, rank: int, bf16: bool = True, stream=None):
+    """Init-time rank-r reconstruction of a float32 [rows, cols] device weight.  Returns
+    (w_r float32, w_r bf16 or None, singular values as a float32 numpy array)."""
+    import numpy as np
+    if w.dtype != torch.float32 or w.dim() != 2 or not w.is_contiguous():
+        raise ValueError("w must be a contiguous float32 matrix")
+    rows, cols = w.shape
+    w_r = torch.empty_like(w)
+    w_b = torch.empty((rows, cols), dtype=torch.bfloat16, device=w.device) if bf16 else None
+    sig = np.zeros(min(rows, cols), np.float32)
+    _check(lib.unstep_svd_truncate(w.data_ptr(), rows, cols, rank, w_r.data_ptr(), _ptr(w_b),
+                                   sig.ctypes.data_as(ctypes.POINTER(_f32)), _stream(stream)))
+    return w_r, w_b, sig
+
+
+def unstep_linear(x: torch.Tensor, w: torch.Tensor, bias: Optional[torch.Tensor] = None,
+                  out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """y = x W^T + b for bf16 x [..., K], W [N, K], b [N]."""
+    for t in (x, w) + ((bias,) if bias is not None else ()):
+        if t.dtype != torch.bfloat16 or not t.is_contiguous():
+            raise ValueError("x, w, bias must be contiguous bf16 tensors")
+    N, K = w.shape
+    if x.shape[-1] != K or (bias is not None and bias.shape != (N,)):
+        raise ValueError("shapes: x [..., K], w [N, K], bias [N]")
+    M = x.numel() // K
+    if out is None:
+        out = torch.empty(x.shape[:-1] + (N,), dtype=torch.bfloat16, device=x.device)
+    _check(lib.unstep_linear(x.data_ptr(), w.data_ptr(), _ptr(bias), out.data_ptr(), M, N, K, _stream(stream)))
+    return out
 
 
 SAMPLERS = {"self_forcing": 0, "unstep": 1, "unstep_one_step": 2}

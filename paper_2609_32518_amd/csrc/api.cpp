@@ -15,6 +15,7 @@
 #include "cache_index.hpp"
 #include "kernels.hpp"
 #include "rope_tables.hpp"
+#include "status.hpp"
 #include "unstep.h"
 
 struct unstep_cache {
@@ -27,28 +28,10 @@ struct unstep_cache {
 
 namespace {
 
-thread_local std::string g_err;
-
-int ok() {
-  g_err.clear();
-  return UNSTEP_OK;
-}
-
-int fail(int code, const char* fmt, ...) {
-  char buf[512];
-  va_list ap;
-  va_start(ap, fmt);
-  vsnprintf(buf, sizeof buf, fmt, ap);
-  va_end(ap);
-  g_err = buf;
-  return code;
-}
-
-int fail_msg(int code, const char* where, const std::string& why) {
-  return fail(code, "%s: %s", where, why.c_str());
-}
-
-bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+using unstep::aligned16;
+using unstep::fail;
+using unstep::fail_msg;
+using unstep::ok;
 
 int check_table_args(const char* where, int32_t f0, int32_t F, int32_t gh, int32_t gw, int32_t D,
                      double theta, const void* c, const void* s) {
@@ -166,7 +149,7 @@ extern "C" {
 
 int unstep_version(void) { return 100; }
 
-const char* unstep_last_error(void) { return g_err.c_str(); }
+const char* unstep_last_error(void) { return unstep::g_err.c_str(); }
 
 int unstep_cache_create(unstep_cache** out, int32_t batch, int32_t n_heads, int32_t head_dim, int32_t grid_h,
                         int32_t grid_w, int32_t sink_frames, int32_t ring_frames, void* k_cache, void* v_cache) {

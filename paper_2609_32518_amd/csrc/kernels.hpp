@@ -71,6 +71,12 @@ struct AttnPlan {
 hipError_t launch_flow_update(const uint16_t* x, const uint16_t* y, uint16_t* out, int64_t n, double a, double b,
                               hipStream_t stream);
 
+// y = bf16(x) on n values, round to nearest even; x and y 16-byte aligned.
+hipError_t launch_cast_bf16(const float* x, uint16_t* y, int64_t n, hipStream_t stream);
+// y = double(x), and y = float(x) rounded to nearest even, on n values.
+hipError_t launch_widen_f64(const float* x, double* y, int64_t n, hipStream_t stream);
+hipError_t launch_narrow_f32(const double* x, float* y, int64_t n, hipStream_t stream);
+
 AttnPlan attn_plan(int32_t B, int32_t H, int32_t N, int32_t n_keys);
 size_t attn_workspace_bytes(int32_t groups);
 hipError_t launch_window_attn(const AttnArgs& a, hipStream_t stream);

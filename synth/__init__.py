@@ -49,6 +49,12 @@ def normal_bf16(shape: Tuple[int, ...], key: Tuple[int, ...], scale: float = 1.0
     return bf16_bits_from_f32(x)
 
 
+def normal_f32(shape: Tuple[int, ...], key: Tuple[int, ...], scale: float = 1.0) -> np.ndarray:
+    """Seeded N(0, scale^2) float32 draw (e.g. a projection weight before its bf16 cast)."""
+    x = generator(*key).standard_normal(size=shape, dtype=np.float32)
+    return (x * np.float32(scale)).astype(np.float32) if scale != 1.0 else x
+
+
 def small_int_bf16(shape: Tuple[int, ...], values: np.ndarray) -> np.ndarray:
     """bf16 bits of small exact integers (|v| < 256), broadcast to `shape`."""
     v = np.broadcast_to(np.asarray(values, dtype=np.float32), shape)

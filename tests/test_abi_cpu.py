@@ -270,3 +270,24 @@ def test_sampler_calls_bit_identical_to_oracle_and_errors():
     assert u.lib.unstep_sampler_calls(1, 2, 3, -1.0, 8, ctypes.byref(n), a, b, c, d, e) == u.OK and n.value == 8
     assert u.lib.unstep_sampler_calls(1, 0, 3, -1.0, 0, ctypes.byref(n), None, None, None, None, None) == u.OK
     assert n.value == 0
+
+
+def test_svd_and_linear_argument_errors():
+    p = FAKE
+    s = (ctypes.c_float * 4)()
+    f = u.lib.unstep_svd_truncate
+    assert f(None, 8, 8, 4, p[1], None, s, None) == u.E_NULL
+    assert f(p[0], 8, 8, 4, None, None, s, None) == u.E_NULL
+    assert f(p[0], 0, 8, 4, p[1], None, s, None) == u.E_SHAPE
+    assert f(p[0], 1 << 15, 1 << 14, 4, p[1], None, s, None) == u.E_SHAPE
+    assert f(p[0], 8, 6, 7, p[1], None, s, None) == u.E_RANGE
+    assert f(p[0], 8, 6, -1, p[1], None, s, None) == u.E_RANGE
+    assert f(p[0] + 4, 8, 8, 4, p[1], None, s, None) == u.E_ALIGN
+    g = u.lib.unstep_linear
+    assert g(None, p[1], None, p[2], 4, 8, 8, None) == u.E_NULL
+    assert g(p[0], p[1], None, None, 4, 8, 8, None) == u.E_NULL
+    assert g(p[0], p[1], None, p[2], 0, 8, 8, None) == u.E_SHAPE
+    assert g(p[0], p[1], None, p[2], 4, 8, 12, None) == u.E_SHAPE
+    assert g(p[0], p[1], None, p[2], 4, 12, 8, None) == u.E_SHAPE
+    assert g(p[0], p[1], p[3] + 2, p[2], 4, 8, 8, None) == u.E_ALIGN
+    assert u.vo_rank(1536) == 1413
