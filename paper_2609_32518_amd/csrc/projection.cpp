@@ -16,8 +16,10 @@
 // unstep_linear: y = x W^T + b in bf16 with float32 accumulation, a plain GEMM with a bias
 // epilogue, run by hipBLASLt.  In column-major terms y^T [N, M] = W [N, K] x^T [K, M]: A = W
 // stored K x N (ld K) with op T, B = x stored K x M (ld K), D = y stored N x M (ld N); the bias
-// runs along D's rows.  Plans (descriptors + chosen algorithm) are cached per device and shape;
-// the first call on a device creates the library handle.
+// runs along D's rows.  Plans (descriptors + chosen algorithm) are cached per device and shape:
+// the first call on a device creates the library handle and a 32 MB workspace, the first call
+// for a shape times hipBLASLt's candidate algorithms on its own operands (synchronising once)
+// and keeps the fastest.
 #include <hip/hip_runtime.h>
 #include <hipblaslt/hipblaslt.h>
 #include <rocblas/rocblas.h>
@@ -73,18 +75,37 @@ hipblasLtHandle_t lt_handle(int dev) {
   return h;
 }
 
-// Called with g_mu held.  Returns nullptr and sets *rc (and the message) when the handle
-// cannot be created or hipBLASLt has no algorithm for the shape.
-const LinearPlan* linear_plan(int dev, int32_t M, int32_t N, int32_t K, bool bias, hipblasLtHandle_t* h_out,
+constexpr size_t kLinearWorkspace = size_t(32) << 20;   // per device, for algorithms that want it
+constexpr int kCandidates = 16;
+
+// Device scratch of the GEMM library, allocated once per device (first call).
+void* lt_workspace(int dev) {
+  static std::map<int, void*> ws;
+  auto it = ws.find(dev);
+  if (it != ws.end()) return it->second;
+  void* p = nullptr;
+  if (hipMalloc(&p, kLinearWorkspace) != hipSuccess) return nullptr;
+  ws[dev] = p;
+  return p;
+}
+
+// Called with g_mu held.  The first call for a (device, shape) asks hipBLASLt for up to
+// kCandidates algorithms, times each on this call's operands (a few runs between events on the
+// call's stream, which synchronises once) and keeps the fastest.  Returns nullptr and sets *rc
+// (and the message) when the handle cannot be created or no algorithm fits the shape.
+const LinearPlan* linear_plan(int dev, int32_t M, int32_t N, int32_t K, const void* x, const void* w,
+                              const void* bias, void* y, hipStream_t st, hipblasLtHandle_t* h_out, void** ws_out,
                               int* rc) {
   static std::map<std::tuple<int, int32_t, int32_t, int32_t, bool>, LinearPlan> plans;
   hipblasLtHandle_t h = lt_handle(dev);
+  void* ws = lt_workspace(dev);
   *h_out = h;
-  if (!h) {
-    *rc = fail(UNSTEP_E_HIP, "unstep_linear: hipblasLtCreate failed");
+  *ws_out = ws;
+  if (!h || !ws) {
+    *rc = fail(UNSTEP_E_HIP, "unstep_linear: creating the GEMM handle or its workspace failed");
     return nullptr;
   }
-  const auto key = std::make_tuple(dev, M, N, K, bias);
+  const auto key = std::make_tuple(dev, M, N, K, bias != nullptr);
   auto it = plans.find(key);
   if (it != plans.end()) return &it->second;
   LinearPlan p;
@@ -101,21 +122,51 @@ const LinearPlan* linear_plan(int dev, int32_t M, int32_t N, int32_t K, bool bia
                        HIPBLAS_STATUS_SUCCESS;
     good = good && hipblasLtMatmulDescSetAttribute(p.desc, HIPBLASLT_MATMUL_DESC_BIAS_DATA_TYPE, &bt, sizeof bt) ==
                        HIPBLAS_STATUS_SUCCESS;
+    good = good && hipblasLtMatmulDescSetAttribute(p.desc, HIPBLASLT_MATMUL_DESC_BIAS_POINTER, &bias, sizeof bias) ==
+                       HIPBLAS_STATUS_SUCCESS;
   }
   good = good && hipblasLtMatrixLayoutCreate(&p.a, HIP_R_16BF, K, N, K) == HIPBLAS_STATUS_SUCCESS;
   good = good && hipblasLtMatrixLayoutCreate(&p.b, HIP_R_16BF, K, M, K) == HIPBLAS_STATUS_SUCCESS;
   good = good && hipblasLtMatrixLayoutCreate(&p.d, HIP_R_16BF, N, M, N) == HIPBLAS_STATUS_SUCCESS;
   hipblasLtMatmulPreference_t pref = nullptr;
   good = good && hipblasLtMatmulPreferenceCreate(&pref) == HIPBLAS_STATUS_SUCCESS;
-  const uint64_t no_workspace = 0;
-  good = good && hipblasLtMatmulPreferenceSetAttribute(pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES,
-                                                        &no_workspace, sizeof no_workspace) == HIPBLAS_STATUS_SUCCESS;
-  hipblasLtMatmulHeuristicResult_t res[1];
+  const uint64_t max_ws = kLinearWorkspace;
+  good = good && hipblasLtMatmulPreferenceSetAttribute(pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES, &max_ws,
+                                                        sizeof max_ws) == HIPBLAS_STATUS_SUCCESS;
+  hipblasLtMatmulHeuristicResult_t res[kCandidates];
   int found = 0;
-  good = good && hipblasLtMatmulAlgoGetHeuristic(h, p.desc, p.a, p.b, p.d, p.d, pref, 1, res, &found) ==
+  good = good && hipblasLtMatmulAlgoGetHeuristic(h, p.desc, p.a, p.b, p.d, p.d, pref, kCandidates, res, &found) ==
                      HIPBLAS_STATUS_SUCCESS;
   if (pref) hipblasLtMatmulPreferenceDestroy(pref);
-  if (!good || found < 1) {
+  // time the candidates on this call's operands
+  int best = -1;
+  float best_ms = 0.f;
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  if (good && found > 1 && hipEventCreate(&e0) == hipSuccess && hipEventCreate(&e1) == hipSuccess) {
+    const float alpha = 1.f, beta = 0.f;
+    for (int i = 0; i < found; ++i) {
+      if (res[i].state != HIPBLAS_STATUS_SUCCESS || res[i].workspaceSize > kLinearWorkspace) continue;
+      bool ran = true;
+      for (int rep = 0; rep < 8 && ran; ++rep) {
+        if (rep == 3) (void)hipEventRecord(e0, st);
+        ran = hipblasLtMatmul(h, p.desc, &alpha, w, p.a, x, p.b, &beta, y, p.d, y, p.d, &res[i].algo, ws,
+                              kLinearWorkspace, st) == HIPBLAS_STATUS_SUCCESS;
+      }
+      float ms = 0.f;
+      if (!ran || hipEventRecord(e1, st) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
+          hipEventElapsedTime(&ms, e0, e1) != hipSuccess)
+        continue;
+      if (best < 0 || ms < best_ms) {
+        best = i;
+        best_ms = ms;
+      }
+    }
+  } else if (good && found == 1) {
+    best = 0;
+  }
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
+  if (!good || best < 0) {
     if (p.a) hipblasLtMatrixLayoutDestroy(p.a);
     if (p.b) hipblasLtMatrixLayoutDestroy(p.b);
     if (p.d) hipblasLtMatrixLayoutDestroy(p.d);
@@ -123,7 +174,7 @@ const LinearPlan* linear_plan(int dev, int32_t M, int32_t N, int32_t K, bool bia
     *rc = fail(UNSTEP_E_SHAPE, "unstep_linear: no hipBLASLt algorithm for M=%d N=%d K=%d", M, N, K);
     return nullptr;
   }
-  p.algo = res[0].algo;
+  p.algo = res[best].algo;
   return &(plans[key] = p);
 }
 
@@ -227,16 +278,18 @@ int unstep_linear(const void* x, const void* w, const void* bias, void* y, int32
   if (e != hipSuccess) return hip_fail(where, e);
   // the plan's descriptor carries the bias pointer: set it and enqueue under the lock
   std::lock_guard<std::mutex> lk(g_mu);
+  hipStream_t st = static_cast<hipStream_t>(hip_stream);
   hipblasLtHandle_t h = nullptr;
+  void* ws = nullptr;
   int rc = UNSTEP_OK;
-  const LinearPlan* p = linear_plan(dev, M, N, K, bias != nullptr, &h, &rc);
+  const LinearPlan* p = linear_plan(dev, M, N, K, x, w, bias, y, st, &h, &ws, &rc);
   if (!p) return rc;
   if (bias && hipblasLtMatmulDescSetAttribute(p->desc, HIPBLASLT_MATMUL_DESC_BIAS_POINTER, &bias, sizeof bias) !=
                   HIPBLAS_STATUS_SUCCESS)
     return fail(UNSTEP_E_HIP, "%s: setting the bias pointer failed", where);
   const float alpha = 1.f, beta = 0.f;
-  if (hipblasLtMatmul(h, p->desc, &alpha, w, p->a, x, p->b, &beta, y, p->d, y, p->d, &p->algo, nullptr, 0,
-                      static_cast<hipStream_t>(hip_stream)) != HIPBLAS_STATUS_SUCCESS)
+  if (hipblasLtMatmul(h, p->desc, &alpha, w, p->a, x, p->b, &beta, y, p->d, y, p->d, &p->algo, ws, kLinearWorkspace,
+                      st) != HIPBLAS_STATUS_SUCCESS)
     return fail(UNSTEP_E_HIP, "%s: hipblasLtMatmul failed", where);
   return ok();
 }
