@@ -1,0 +1,122 @@
+"""GPU edge cases of the chunk step through the C ABI: a single token attending to a single
+key, a zero window with sinks, and a cache at the maximum size the ABI accepts (just under
+2^31 bytes per (batch, head) buffer) whose ring has wrapped, checked against closed forms the
+oracle's cache model gives (every retained key equally weighted; one dominant needle key far
+out in the buffer, which also drives the work-group's exact-max fallback).
+Inputs from synth or closed-form recipes; expected values from oracle only."""
+import math
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import numerics
+from oracle.kvcache import KVCacheOracle, retained_frames, slot_of_frame
+from tests.gpu_helpers import Mirror, check_attention, host, log
+
+pytestmark = pytest.mark.gpu
+
+u = pytest.importorskip("paper_2609_32518_amd")
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+SCALE = 1.0 / math.sqrt(128.0)
+
+
+def test_single_token_single_key():
+    # grid 1x1, one-frame chunks, no window: each query sees exactly its own key, so the output
+    # is that key's value row, bit for bit, and the log-sum-exp is the scaled score
+    m = Mirror(u, 1, 1, 1, 1, 0, 1)
+    for f in range(3):
+        q_rot, out, lse, q_want = m.step(f, 1, 0, (40, f), lse=True)
+        torch.cuda.synchronize()
+        assert np.array_equal(host(q_rot), q_want)
+        m.check_cache(f"frame {f}")
+        v_row = m.orc.v[0, 0, m.orc.slot(f)]
+        assert np.array_equal(host(out).reshape(-1), v_row)
+        s = float(np.dot(numerics.bf16_to_f64(q_want.reshape(-1)), numerics.bf16_to_f64(m.orc.k[0, 0, m.orc.slot(f)])))
+        assert abs(float(lse.cpu().numpy().reshape(-1)[0]) - s * SCALE) <= 1e-5 * max(1.0, abs(s * SCALE))
+
+
+def test_zero_window_keeps_sinks_and_chunk():
+    m = Mirror(u, 1, 2, 4, 6, 2, 3)
+    for c in range(5):
+        q_rot, out, _, q_want = m.step(2 * c, 2, 0, (41, c))
+        torch.cuda.synchronize()
+        m.check_cache(f"chunk {c}")
+        assert m.orc.retained(2 * c, 2, 0) == sorted(set(range(min(2, 2 * c))) | {2 * c, 2 * c + 1})
+        want, _ = m.expected(q_want, 2 * c, 2, 0)
+        check_attention(host(out), want, f"chunk {c}")
+
+
+def _v_pattern(frames: np.ndarray) -> np.ndarray:
+    # value row of every token of frame f: ((3 f + d) mod 8) - 3.5, exact in bf16
+    d = np.arange(128)
+    return ((3 * frames[:, None] + d[None, :]) % 8).astype(np.float64) - 3.5
+
+
+def test_maximum_cache_with_wrapped_ring():
+    # 64x64 tokens per frame, a ring of 2047 frames: 8,384,512 rows per buffer, the last byte at
+    # 2^31 - 1,048,833; the chunk at frame 3047 sees frames 1001-3047 through a wrapped ring
+    gh = gw = 64
+    T = gh * gw
+    R = 2047
+    f0 = 3047
+    W = R - 1
+    rows = R * T
+    assert rows <= 8388607 and rows * 256 < 2 ** 31
+    k_buf = torch.zeros((1, 1, rows, 128), dtype=torch.bfloat16, device="cuda")
+    v_buf = torch.empty((1, 1, rows, 128), dtype=torch.bfloat16, device="cuda")
+    cache = u.Cache(1, 1, gh, gw, 0, R, k_cache=k_buf, v_cache=v_buf)
+    orc = KVCacheOracle(1, 1, 128, 1, 1, 0, R)       # index model only (one token per frame)
+    for start in range(0, f0, R):
+        n = min(R, f0 - start)
+        cache.advance(start, n)
+        orc.append(start, n, np.zeros((1, n, 1, 128), np.uint16), np.zeros((1, n, 1, 128), np.uint16))
+    fm, newest = cache.frame_map()
+    assert fm == orc.frame_of_slot and newest == f0 - 1
+    # value rows of every slot from the frame it holds (device fill from the same recipe)
+    pat = torch.from_numpy(_v_pattern(np.array(fm, dtype=np.int64))).to("cuda", torch.bfloat16)   # [R, 128]
+    v_buf.view(R, T, 128).copy_(pat[:, None, :].expand(R, T, 128))
+    # the chunk: zero keys, pattern values, appended through the library (no queries)
+    tables = u.RopeTableCache("cuda")
+    cos_t, sin_t = tables.get(f0, 1, gh, gw)
+    kz = torch.zeros((1, T, 1, 128), dtype=torch.bfloat16, device="cuda")
+    vc = pat.new_tensor(_v_pattern(np.array([f0]))).to(torch.bfloat16).expand(T, 128).reshape(1, T, 1, 128).contiguous()
+    cache.unstep_kv_append(f0, 1, None, kz, vc, cos_t, sin_t)
+    orc.append(f0, 1, np.zeros((1, 1, 1, 128), np.uint16), np.zeros((1, 1, 1, 128), np.uint16))
+    frames = retained_frames(f0, 1, 0, W)
+    assert frames == list(range(f0 - W, f0 + 1)) and len(cache.segments(f0, 1, W)) == 2
+    n_keys = len(frames) * T
+    vals = _v_pattern(np.array(frames))                              # [frames, 128]
+    log(f"max cache: {rows} rows per buffer, {n_keys} keys, {len(cache.segments(f0, 1, W))} segments")
+
+    # (a) zero queries: every retained key weighs the same, the output is their mean value row
+    q0 = torch.zeros((1, T, 1, 128), dtype=torch.bfloat16, device="cuda")
+    out = cache.unstep_window_attn(f0, 1, W, q0)
+    torch.cuda.synchronize()
+    want = vals.mean(axis=0)
+    got = numerics.bf16_to_f64(host(out)).reshape(T, 128)
+    assert np.abs(got - want[None, :]).max() <= 2.0 ** -8 * np.abs(want).max() + 1e-3
+
+    # (b) a needle: the last token of the slot nearest the end of the buffer gets key e_0 * kv,
+    # every query is e_0 * qv, all other keys are zero; its weight dominates the sum
+    slot = R - 1
+    f_needle = fm[slot]
+    assert f_needle in frames and slot_of_frame(f_needle, 0, R) == slot
+    kv, qv = 24.0, 24.0     # score 576: exp(50.9) against 8.4M unit weights; 2^73 > 2^64 forces the exact-max redo
+    k_buf[0, 0, (slot + 1) * T - 1, 0] = kv
+    v_buf[0, 0, (slot + 1) * T - 1] = torch.full((128,), 3.0, dtype=torch.bfloat16)
+    q = torch.zeros((1, T, 1, 128), dtype=torch.bfloat16, device="cuda")
+    q[..., 0] = qv
+    lse = torch.empty((1, 1, T), dtype=torch.float32, device="cuda")
+    out = cache.unstep_window_attn(f0, 1, W, q, lse=lse)
+    torch.cuda.synchronize()
+    a = kv * qv * SCALE
+    others = vals.sum(axis=0) * T - _v_pattern(np.array([f_needle]))[0]
+    want = (math.exp(a) * 3.0 + others) / (math.exp(a) + n_keys - 1)
+    got = numerics.bf16_to_f64(host(out)).reshape(T, 128)
+    log(f"needle: weight {math.exp(a) / (math.exp(a) + n_keys - 1):.6f}, max err {np.abs(got - want).max():.3g}")
+    assert np.abs(got - want[None, :]).max() <= 2.0 ** -8 * 3.0 + 1e-3
+    want_lse = math.log(math.exp(a) + n_keys - 1)
+    assert np.abs(lse.cpu().numpy() - want_lse).max() <= 1e-3
