@@ -40,6 +40,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <cfloat>
 #include <climits>
 
 #include "kernels.hpp"
@@ -506,11 +507,13 @@ __global__ __launch_bounds__(kThreads) void window_attn_kernel(AttnArgs a) {
 }
 
 // Finish every query tile whose key range was shared by several work-groups: merge their
-// partials by log-sum-exp, out = sum_p w_p o_p / sum_p w_p with w_p = l_p 2^((m_p - M) c2),
-// M = max_p m_p.  Work-group = (query tile, 8 rows), thread = (row, 4 output columns), so the
-// schedule arithmetic (64-bit divisions) is work-group uniform and runs once per wave on the
-// scalar unit, and each wave reads two whole 512-byte partial rows per load instruction.
-constexpr int kCombineRows = 8;
+// partials by log-sum-exp in one pass, keeping a running offset M: each partial (m, l, o)
+// rescales the sums by 2^((M_old - M) c2) when it raises M and adds w = l 2^((m - M) c2),
+// out = sum w o / sum w.  Work-group = (query tile, 32 rows), thread = (4 rows, 4 output
+// columns): the schedule arithmetic (64-bit divisions) is work-group uniform and runs on the
+// scalar unit, and each thread keeps the loads of 4 rows in flight.
+constexpr int kCombineRowsPerThread = 4;
+constexpr int kCombineRows = 8 * kCombineRowsPerThread;   // rows per work-group
 
 __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
   int32_t qtiles;
@@ -518,44 +521,61 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
   constexpr int kGroupsPerTile = kBlockQ / kCombineRows;
   const int64_t t = blockIdx.x / kGroupsPerTile;                       // (b, h, query tile)
   const int32_t qt = int32_t(t % qtiles);
-  const int32_t r = int32_t(blockIdx.x % kGroupsPerTile) * kCombineRows + int32_t(threadIdx.x >> 5);
+  const int32_t r0 = int32_t(blockIdx.x % kGroupsPerTile) * kCombineRows + int32_t(threadIdx.x >> 5);
   const int32_t part = threadIdx.x & 31;
-  const int32_t qi = qt * kBlockQ + r;
   const int64_t ua = t * sc.Tk;
   const int64_t ga = sc.owner(ua), gb = sc.owner(ua + sc.Tk - 1);
-  if (ga == gb || qi >= a.N) return;                                  // written directly by its work-group
+  if (ga == gb) return;                                              // written directly by its work-group
   const float c2 = a.scale * kLog2e;
-  float M = -INFINITY;
-  for (int64_t g = ga; g <= gb; ++g) {
-    const int64_t prow = (g * 2 + (sc.start(g) >= ua ? 0 : 1)) * kBlockQ + r;
-    if (a.part_ml[prow * 2 + 1] > 0.f) M = fmaxf(M, a.part_ml[prow * 2]);
+  float M[kCombineRowsPerThread], W[kCombineRowsPerThread];
+  float4 acc[kCombineRowsPerThread];
+#pragma unroll
+  for (int j = 0; j < kCombineRowsPerThread; ++j) {
+    M[j] = -FLT_MAX;
+    W[j] = 0.f;
+    acc[j] = make_float4(0.f, 0.f, 0.f, 0.f);
   }
-  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  float wsum = 0.f;
   for (int64_t g = ga; g <= gb; ++g) {
-    const int64_t prow = (g * 2 + (sc.start(g) >= ua ? 0 : 1)) * kBlockQ + r;
-    const float m = a.part_ml[prow * 2];
-    const float l = a.part_ml[prow * 2 + 1];
-    if (!(l > 0.f)) continue;
-    const float wgt = l * __builtin_amdgcn_exp2f((m - M) * c2);
-    const float4 v = *reinterpret_cast<const float4*>(a.part_o + prow * kHeadDim + part * 4);
-    acc.x += wgt * v.x;
-    acc.y += wgt * v.y;
-    acc.z += wgt * v.z;
-    acc.w += wgt * v.w;
-    wsum += wgt;
+    const int64_t base = (g * 2 + (sc.start(g) >= ua ? 0 : 1)) * kBlockQ + r0;
+    float2 ml[kCombineRowsPerThread];
+    float4 v[kCombineRowsPerThread];
+#pragma unroll
+    for (int j = 0; j < kCombineRowsPerThread; ++j) {
+      const int64_t prow = base + 8 * j;
+      ml[j] = *reinterpret_cast<const float2*>(a.part_ml + prow * 2);
+      v[j] = *reinterpret_cast<const float4*>(a.part_o + prow * kHeadDim + part * 4);
+    }
+#pragma unroll
+    for (int j = 0; j < kCombineRowsPerThread; ++j) {
+      const float l = ml[j].y > 0.f ? ml[j].y : 0.f;              // an empty partial adds nothing
+      const float m = ml[j].y > 0.f ? ml[j].x : -FLT_MAX;
+      const float mn = fmaxf(M[j], m);
+      const float s_old = __builtin_amdgcn_exp2f((M[j] - mn) * c2);
+      const float w = l * __builtin_amdgcn_exp2f((m - mn) * c2);
+      acc[j].x = acc[j].x * s_old + w * v[j].x;
+      acc[j].y = acc[j].y * s_old + w * v[j].y;
+      acc[j].z = acc[j].z * s_old + w * v[j].z;
+      acc[j].w = acc[j].w * s_old + w * v[j].w;
+      W[j] = W[j] * s_old + w;
+      M[j] = mn;
+    }
   }
-  const float inv = 1.f / wsum;
   const int32_t bh_idx = int32_t(t / qtiles);
   const int32_t h = bh_idx % a.H, b = bh_idx / a.H;
   typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
-  bf16x4_t o;
-  o[0] = (__bf16)(acc.x * inv);
-  o[1] = (__bf16)(acc.y * inv);
-  o[2] = (__bf16)(acc.z * inv);
-  o[3] = (__bf16)(acc.w * inv);
-  *reinterpret_cast<bf16x4_t*>(a.out + ((int64_t(b) * a.N + qi) * a.H + h) * kHeadDim + part * 4) = o;
-  if (a.lse && part == 0) a.lse[(int64_t(b) * a.H + h) * a.N + qi] = M * a.scale + logf(wsum);
+#pragma unroll
+  for (int j = 0; j < kCombineRowsPerThread; ++j) {
+    const int32_t qi = qt * kBlockQ + r0 + 8 * j;
+    if (qi >= a.N) break;
+    const float inv = 1.f / W[j];
+    bf16x4_t o;
+    o[0] = (__bf16)(acc[j].x * inv);
+    o[1] = (__bf16)(acc[j].y * inv);
+    o[2] = (__bf16)(acc[j].z * inv);
+    o[3] = (__bf16)(acc[j].w * inv);
+    *reinterpret_cast<bf16x4_t*>(a.out + ((int64_t(b) * a.N + qi) * a.H + h) * kHeadDim + part * 4) = o;
+    if (a.lse && part == 0) a.lse[(int64_t(b) * a.H + h) * a.N + qi] = M[j] * a.scale + logf(W[j]);
+  }
 }
 
 }  // namespace
@@ -563,20 +583,22 @@ __global__ __launch_bounds__(256) void attn_combine_kernel(AttnArgs a) {
 AttnPlan attn_plan(int32_t B, int32_t H, int32_t N, int32_t n_keys) {
   // Plain: one work-group per query tile over its whole key range.  Balanced: one
   // work-group per compute unit (256 CUs) shares all (query tile, key tile) units equally,
-  // and query tiles cut between work-groups are merged by attn_combine.  Estimated times
-  // (us): a work-group's 256-query x 64-key tile ~1.6; partials (fp32, written and read
-  // back) at ~5 TB/s plus ~5 us for the extra launch.
+  // and query tiles cut between work-groups are merged by attn_combine.  Costs measured on
+  // MI355X (us): a 256-query x 64-key tile takes ~1.66 when a work-group walks one query
+  // tile's whole range and ~1.82 per unit in the balanced schedule (two segments per
+  // work-group, fp32 partials written, and all compute units drawing power, which lowers the
+  // clock of the power-limited chip); the merge reads the partials at ~4.5 TB/s plus ~2 us.
   constexpr int64_t kSlots = 256;
-  constexpr double kTileUs = 1.6;
+  constexpr double kTileUsPlain = 1.66, kTileUsBalanced = 1.82;
   const int64_t qtiles = int64_t(B) * H * ((N + kBlockQ - 1) / kBlockQ);
   const int64_t tk = (n_keys + kBlockK - 1) / kBlockK;
   const int64_t units = qtiles * tk;
   AttnPlan plain{int32_t(qtiles), 0, int32_t(qtiles), 0};
   const int64_t g = std::min<int64_t>(kSlots, units / 4);
   if (g <= qtiles) return plain;
-  const double t_plain = double((qtiles + kSlots - 1) / kSlots) * double(tk) * kTileUs;
+  const double t_plain = double((qtiles + kSlots - 1) / kSlots) * double(tk) * kTileUsPlain;
   const size_t ws = attn_workspace_bytes(int32_t(g));
-  const double t_bal = double((units + g - 1) / g) * kTileUs + double(ws) * 2.0 / 5.0e6 + 5.0;
+  const double t_bal = double((units + g - 1) / g) * kTileUsBalanced + double(ws) / 4.5e6 + 2.0;
   if (t_bal >= t_plain) return plain;
   return AttnPlan{int32_t(g), ws, int32_t(qtiles), size_t(g) * 2 * kBlockQ * kHeadDim};
 }
