@@ -359,6 +359,17 @@ def summarize_profile(d, workload="full_chunk", qknorm=False):
     for r in stats[:6]:
         lines.append(f"| {kname(r['Name'])} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
                      f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.1f} |")
+    # the bench's own per-kernel timing launches each kernel `steps` times back to back at the
+    # end of the run: the same dispatches' average, for comparison with its HIP-event figure
+    trace_rows = sorted(csv.DictReader(open(os.path.join(d, "trace", "trace_kernel_trace.csv"))),
+                        key=lambda r: int(r["Start_Timestamp"]))
+    steps = 30
+    for kern in ("window_attn_kernel", "rope_append_kernel<true>", "rope_norm_append_kernel<true, 3>"):
+        durs = [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in trace_rows if kname(r["Kernel_Name"]) == kern]
+        if len(durs) >= steps:
+            tail = durs[-steps:]
+            lines.append(f"\n{kern}: the last {steps} dispatches (the bench's back-to-back per-kernel timing loop) "
+                         f"average {sum(tail) / len(tail) / 1e3:.2f} µs.")
     lines += ["", "## HBM traffic per dispatch (rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE)", "",
               f"Scale factors from a plain 256 MB device copy (`--copy-calibration 256`): FETCH_SIZE read "
               f"{copy_f:.0f} KiB -> x{f_scale:.3f}; WRITE_SIZE read {copy_w:.0f} KiB -> x{w_scale:.3f}.", "",
