@@ -142,11 +142,18 @@ struct Walk {
 // key kt0 into the tile at LDS address dst: lane l of instruction i lands in row lrow + 4 i,
 // physical slot l & 15, and so fetches logical piece (l & 15) ^ swz(row).  Keys past the
 // range read the range's last key (finite values; their scores are masked to -inf).
+// kOneRun: the walk's whole range lies in the segment table's first run (a cache that has not
+// wrapped and holds no separate sinks), so rows follow keys with no table lookup; this keeps
+// the scalar work of the V phase, which shares the wave's issue slots with its softmax, small.
 // Written as inline assembly: M0 holds the wave's LDS destination, the lane's 16 bytes land
 // at M0 + 16 l.
+template <bool kOneRun>
 __device__ __forceinline__ void load_rows(uint32_t dst, const uint8_t* base, const Walk& w, int wave, int32_t kt0) {
   int32_t rows[2];
-  if (kt0 + kBlockK <= min(w.seg.run_end(kt0), w.k_end)) {      // whole tile inside one run
+  if (kOneRun) {                 // the whole range lies in the first run: rows follow keys
+#pragma unroll
+    for (int i = 0; i < 2; ++i) rows[i] = min(kt0 + w.lrow + 4 * i, w.k_end - 1) + w.seg.r0;
+  } else if (kt0 + kBlockK <= min(w.seg.run_end(kt0), w.k_end)) {      // whole tile inside one run
     const int32_t r0 = w.seg.row(kt0);
     rows[0] = r0 + w.lrow;
     rows[1] = r0 + w.lrow + 4;
@@ -165,10 +172,11 @@ __device__ __forceinline__ void load_rows(uint32_t dst, const uint8_t* base, con
 // Stage t into ring slot `slot`: K tile t and V tile t - 1.  The first and last stages hold
 // only one of them; the other half is filled with a duplicate tile so that every stage
 // costs each wave the same number of loads (the in-flight accounting counts loads).
+template <bool kOneRun>
 __device__ __forceinline__ void load_stage(int slot, const Walk& w, int wave, int32_t t) {
   const int32_t tk = min(t, w.n - 1), tv = max(t - 1, 0);
-  load_rows(w.lds_k + slot * kTileBytes, w.kbase, w, wave, w.k_begin + tk * kBlockK);
-  load_rows(w.lds_v + slot * kTileBytes, w.vbase, w, wave, w.k_begin + tv * kBlockK);
+  load_rows<kOneRun>(w.lds_k + slot * kTileBytes, w.kbase, w, wave, w.k_begin + tk * kBlockK);
+  load_rows<kOneRun>(w.lds_v + slot * kTileBytes, w.vbase, w, wave, w.k_begin + tv * kBlockK);
 }
 
 // Register state of one wave.
@@ -248,12 +256,12 @@ __device__ __forceinline__ void m_phase(Acc& a, int slot, const bf16x8_t (&qf)[8
 // V phase of tile t: mask keys past the range (last tile), the exponent offsets (first
 // tile of pass 0), then P and its row sums (kMode 2: only the row max), with this wave's
 // share of the loads of stage t + 3 issued before and after the arithmetic.
-template <int kMode, int kLoadSlot>
+template <int kMode, int kLoadSlot, bool kOneRun>
 __device__ __forceinline__ void v_phase(Acc& a, int32_t t, const Walk& w, int wave) {
   // this wave's share of stage t + 3 (K tile t + 3, V tile t + 2) into the slot that held
   // stage t - 1
   const bool load = t + kAhead <= w.n;
-  if (load) load_rows(w.lds_k + kLoadSlot * kTileBytes, w.kbase, w, wave, w.k_begin + min(t + kAhead, w.n - 1) * kBlockK);
+  if (load) load_rows<kOneRun>(w.lds_k + kLoadSlot * kTileBytes, w.kbase, w, wave, w.k_begin + min(t + kAhead, w.n - 1) * kBlockK);
   const int32_t kt0 = w.k_begin + t * kBlockK;
   if (kt0 + kBlockK > w.k_end) {
 #pragma unroll
@@ -265,7 +273,7 @@ __device__ __forceinline__ void v_phase(Acc& a, int32_t t, const Walk& w, int wa
   if (kMode == 2) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) a.mx = fmaxf(a.mx, fmaxf(a.s[0][i], a.s[1][i]));
-    if (load) load_rows(w.lds_v + kLoadSlot * kTileBytes, w.vbase, w, wave, w.k_begin + (t + kAhead - 1) * kBlockK);
+    if (load) load_rows<kOneRun>(w.lds_v + kLoadSlot * kTileBytes, w.vbase, w, wave, w.k_begin + (t + kAhead - 1) * kBlockK);
     return;
   }
   if (kMode == 0 && t == 0) {
@@ -288,7 +296,7 @@ __device__ __forceinline__ void v_phase(Acc& a, int32_t t, const Walk& w, int wa
       a.p[kb][i >> 3][(i & 7) + 1] = (__bf16)e1;
     }
   a.l += acc0 + acc1;
-  if (load) load_rows(w.lds_v + kLoadSlot * kTileBytes, w.vbase, w, wave, w.k_begin + (t + kAhead - 1) * kBlockK);
+  if (load) load_rows<kOneRun>(w.lds_v + kLoadSlot * kTileBytes, w.vbase, w, wave, w.k_begin + (t + kAhead - 1) * kBlockK);
 }
 
 // Tile t of the walk, with stage t in ring slot kSlot: the M phase of tile t, the stage
@@ -301,21 +309,21 @@ __device__ __forceinline__ void v_phase(Acc& a, int32_t t, const Walk& w, int wa
 // for everyone when phase 2t + 2 (group A's M phase of tile t + 1) starts.  The slot
 // refilled with stage t + 3 (group A in phase 2t + 1, group B in 2t + 2) last held stage
 // t - 1, read by group B in global phase 2t - 1.
-template <int kMode, int kSlot>
+template <int kMode, int kSlot, bool kOneRun>
 __device__ __forceinline__ void step(Acc& a, const Walk& w, const bf16x8_t (&qf)[8], int wave, int32_t t) {
   if (t > w.n) return;
   constexpr int kLoadSlot = (kSlot + kAhead) % kStages;
   m_phase(a, kSlot, qf, w);
   if (t + 1 <= w.n) wait_stages_in_flight(min(kAhead - 2, w.n - t - 1));
   barrier();
-  if (t < w.n) v_phase<kMode, kLoadSlot>(a, t, w, wave);
+  if (t < w.n) v_phase<kMode, kLoadSlot, kOneRun>(a, t, w, wave);
   barrier();
 }
 
 // One walk over the key range.  kMode 0: exponent offsets from the first tile (pass 0);
 // 1: offsets given in a.m_off; 2: exact row max only (a.mx).  Accumulates O^T and the row
 // sums from zero (modes 0 and 1).
-template <int kMode>
+template <int kMode, bool kOneRun>
 __device__ __forceinline__ void walk(Acc& a, const Walk& w, const bf16x8_t (&qf)[8], int wave, int group) {
   const f32x16_t zero = {};
 #pragma unroll
@@ -333,15 +341,15 @@ __device__ __forceinline__ void walk(Acc& a, const Walk& w, const bf16x8_t (&qf)
   barrier();                                   // the ring is free
 #pragma unroll
   for (int t = 0; t < kAhead; ++t)
-    if (t <= w.n) load_stage(t, w, wave, t);
+    if (t <= w.n) load_stage<kOneRun>(t, w, wave, t);
   wait_stages_in_flight(min(kAhead - 1, w.n));
   barrier();                                   // stage 0 is complete: global phase 0
   if (group == 1) barrier();                   // group B idles in phase 0
   for (int32_t t0 = 0; t0 <= w.n; t0 += kStages) {
-    step<kMode, 0>(a, w, qf, wave, t0);
-    step<kMode, 1>(a, w, qf, wave, t0 + 1);
-    step<kMode, 2>(a, w, qf, wave, t0 + 2);
-    step<kMode, 3>(a, w, qf, wave, t0 + 3);
+    step<kMode, 0, kOneRun>(a, w, qf, wave, t0);
+    step<kMode, 1, kOneRun>(a, w, qf, wave, t0 + 1);
+    step<kMode, 2, kOneRun>(a, w, qf, wave, t0 + 2);
+    step<kMode, 3, kOneRun>(a, w, qf, wave, t0 + 3);
   }
   if (group == 0) barrier();                   // group A idles in the last phase
 }
@@ -461,11 +469,21 @@ __global__ __launch_bounds__(kThreads) void window_attn_kernel(AttnArgs a) {
     // segment with the exact row max, where no probability exceeds 1.
     Acc acc;
     acc.m_off = 0.f;
-    walk<0>(acc, w, qf, wave, group);
-    if (__syncthreads_or(!(acc.l <= 0x1p64f))) {
-      walk<2>(acc, w, qf, wave, group);
-      acc.m_off = fmaxf(acc.mx, __shfl_xor(acc.mx, 32));
-      walk<1>(acc, w, qf, wave, group);
+    // a range inside the first run of the segment table takes the loader's branch-free path
+    if (w.k_end <= w.seg.l1) {
+      walk<0, true>(acc, w, qf, wave, group);
+      if (__syncthreads_or(!(acc.l <= 0x1p64f))) {
+        walk<2, true>(acc, w, qf, wave, group);
+        acc.m_off = fmaxf(acc.mx, __shfl_xor(acc.mx, 32));
+        walk<1, true>(acc, w, qf, wave, group);
+      }
+    } else {
+      walk<0, false>(acc, w, qf, wave, group);
+      if (__syncthreads_or(!(acc.l <= 0x1p64f))) {
+        walk<2, false>(acc, w, qf, wave, group);
+        acc.m_off = fmaxf(acc.mx, __shfl_xor(acc.mx, 32));
+        walk<1, false>(acc, w, qf, wave, group);
+      }
     }
 
     // ---- segment epilogue: the final output, or a partial for the combine pass
