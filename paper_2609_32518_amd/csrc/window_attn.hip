@@ -93,6 +93,10 @@ struct SegTable {
   __device__ __forceinline__ int32_t run_end(int32_t key) const {
     return key < l1 ? l1 : key < l2 ? l2 : key < l3 ? l3 : INT32_MAX;
   }
+  // Logical start of the run holding key.
+  __device__ __forceinline__ int32_t run_start(int32_t key) const {
+    return key >= l3 ? l3 : key >= l2 ? l2 : key >= l1 ? l1 : 0;
+  }
 };
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t u) { return __builtin_bit_cast(bf16x8_t, u); }
@@ -131,6 +135,9 @@ struct Walk {
   int32_t n;                   // tiles in the range
   int half;
   int lrow;                    // loader: tile row of this lane in its first load (+4)
+  // loader cursors of walks over several runs, one for K tiles and one for V tiles: a tile
+  // whose keys [kt0, kt0 + 64) lie in [lo, hi) maps key kt0 to row kt0 + delta
+  int32_t kc_lo, kc_hi, kc_delta, vc_lo, vc_hi, vc_delta;
   int lpiece[2];               // loader: byte offset of this lane's logical 16-byte piece
   uint32_t lds_k, lds_v;       // LDS address of ring slot 0's K tile and V tile (uniform)
   uint32_t koff[8];            // LDS address of the K fragment for d-step 0..7 in slot 0
@@ -143,23 +150,31 @@ struct Walk {
 // physical slot l & 15, and so fetches logical piece (l & 15) ^ swz(row).  Keys past the
 // range read the range's last key (finite values; their scores are masked to -inf).
 // kOneRun: the walk's whole range lies in the segment table's first run (a cache that has not
-// wrapped and holds no separate sinks), so rows follow keys with no table lookup; this keeps
-// the scalar work of the V phase, which shares the wave's issue slots with its softmax, small.
+// wrapped and holds no separate sinks), so rows follow keys with no table lookup.  Otherwise a
+// cursor (lo, hi, delta) per operand remembers the run of the last tile it mapped: a tile
+// inside it costs two scalar compares, and only a tile that crosses a run boundary or the
+// range's end looks rows up per lane and moves the cursor to the run of the tile after it.
+// Both keep the scalar work of the V phase, which shares the wave's issue slots with its
+// softmax, small.
 // Written as inline assembly: M0 holds the wave's LDS destination, the lane's 16 bytes land
 // at M0 + 16 l.
 template <bool kOneRun>
-__device__ __forceinline__ void load_rows(uint32_t dst, const uint8_t* base, const Walk& w, int wave, int32_t kt0) {
+__device__ __forceinline__ void load_rows(uint32_t dst, const uint8_t* base, const Walk& w, int32_t& c_lo,
+                                          int32_t& c_hi, int32_t& c_delta, int wave, int32_t kt0) {
   int32_t rows[2];
   if (kOneRun) {                 // the whole range lies in the first run: rows follow keys
 #pragma unroll
     for (int i = 0; i < 2; ++i) rows[i] = min(kt0 + w.lrow + 4 * i, w.k_end - 1) + w.seg.r0;
-  } else if (kt0 + kBlockK <= min(w.seg.run_end(kt0), w.k_end)) {      // whole tile inside one run
-    const int32_t r0 = w.seg.row(kt0);
-    rows[0] = r0 + w.lrow;
-    rows[1] = r0 + w.lrow + 4;
-  } else {
+  } else if (kt0 >= c_lo && kt0 + kBlockK <= c_hi) {     // whole tile inside the cursor's run
+    rows[0] = kt0 + c_delta + w.lrow;
+    rows[1] = rows[0] + 4;
+  } else {                       // crosses a run boundary or the range's end: per-lane lookup
 #pragma unroll
     for (int i = 0; i < 2; ++i) rows[i] = w.seg.row(min(kt0 + w.lrow + 4 * i, w.k_end - 1));
+    const int32_t nx = kt0 + kBlockK;       // move the cursor to the run of the next tile
+    c_lo = w.seg.run_start(nx);
+    c_hi = min(w.seg.run_end(nx), w.k_end);
+    c_delta = w.seg.row(nx) - nx;
   }
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
@@ -173,10 +188,12 @@ __device__ __forceinline__ void load_rows(uint32_t dst, const uint8_t* base, con
 // only one of them; the other half is filled with a duplicate tile so that every stage
 // costs each wave the same number of loads (the in-flight accounting counts loads).
 template <bool kOneRun>
-__device__ __forceinline__ void load_stage(int slot, const Walk& w, int wave, int32_t t) {
+__device__ __forceinline__ void load_stage(int slot, Walk& w, int wave, int32_t t) {
   const int32_t tk = min(t, w.n - 1), tv = max(t - 1, 0);
-  load_rows<kOneRun>(w.lds_k + slot * kTileBytes, w.kbase, w, wave, w.k_begin + tk * kBlockK);
-  load_rows<kOneRun>(w.lds_v + slot * kTileBytes, w.vbase, w, wave, w.k_begin + tv * kBlockK);
+  load_rows<kOneRun>(w.lds_k + slot * kTileBytes, w.kbase, w, w.kc_lo, w.kc_hi, w.kc_delta, wave,
+                     w.k_begin + tk * kBlockK);
+  load_rows<kOneRun>(w.lds_v + slot * kTileBytes, w.vbase, w, w.vc_lo, w.vc_hi, w.vc_delta, wave,
+                     w.k_begin + tv * kBlockK);
 }
 
 // Register state of one wave.
@@ -257,11 +274,11 @@ __device__ __forceinline__ void m_phase(Acc& a, int slot, const bf16x8_t (&qf)[8
 // tile of pass 0), then P and its row sums (kMode 2: only the row max), with this wave's
 // share of the loads of stage t + 3 issued before and after the arithmetic.
 template <int kMode, int kLoadSlot, bool kOneRun>
-__device__ __forceinline__ void v_phase(Acc& a, int32_t t, const Walk& w, int wave) {
+__device__ __forceinline__ void v_phase(Acc& a, int32_t t, Walk& w, int wave) {
   // this wave's share of stage t + 3 (K tile t + 3, V tile t + 2) into the slot that held
   // stage t - 1
   const bool load = t + kAhead <= w.n;
-  if (load) load_rows<kOneRun>(w.lds_k + kLoadSlot * kTileBytes, w.kbase, w, wave, w.k_begin + min(t + kAhead, w.n - 1) * kBlockK);
+  if (load) load_rows<kOneRun>(w.lds_k + kLoadSlot * kTileBytes, w.kbase, w, w.kc_lo, w.kc_hi, w.kc_delta, wave, w.k_begin + min(t + kAhead, w.n - 1) * kBlockK);
   const int32_t kt0 = w.k_begin + t * kBlockK;
   if (kt0 + kBlockK > w.k_end) {
 #pragma unroll
@@ -273,7 +290,7 @@ __device__ __forceinline__ void v_phase(Acc& a, int32_t t, const Walk& w, int wa
   if (kMode == 2) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) a.mx = fmaxf(a.mx, fmaxf(a.s[0][i], a.s[1][i]));
-    if (load) load_rows<kOneRun>(w.lds_v + kLoadSlot * kTileBytes, w.vbase, w, wave, w.k_begin + (t + kAhead - 1) * kBlockK);
+    if (load) load_rows<kOneRun>(w.lds_v + kLoadSlot * kTileBytes, w.vbase, w, w.vc_lo, w.vc_hi, w.vc_delta, wave, w.k_begin + (t + kAhead - 1) * kBlockK);
     return;
   }
   if (kMode == 0 && t == 0) {
@@ -296,7 +313,7 @@ __device__ __forceinline__ void v_phase(Acc& a, int32_t t, const Walk& w, int wa
       a.p[kb][i >> 3][(i & 7) + 1] = (__bf16)e1;
     }
   a.l += acc0 + acc1;
-  if (load) load_rows<kOneRun>(w.lds_v + kLoadSlot * kTileBytes, w.vbase, w, wave, w.k_begin + (t + kAhead - 1) * kBlockK);
+  if (load) load_rows<kOneRun>(w.lds_v + kLoadSlot * kTileBytes, w.vbase, w, w.vc_lo, w.vc_hi, w.vc_delta, wave, w.k_begin + (t + kAhead - 1) * kBlockK);
 }
 
 // Tile t of the walk, with stage t in ring slot kSlot: the M phase of tile t, the stage
@@ -310,7 +327,7 @@ __device__ __forceinline__ void v_phase(Acc& a, int32_t t, const Walk& w, int wa
 // refilled with stage t + 3 (group A in phase 2t + 1, group B in 2t + 2) last held stage
 // t - 1, read by group B in global phase 2t - 1.
 template <int kMode, int kSlot, bool kOneRun>
-__device__ __forceinline__ void step(Acc& a, const Walk& w, const bf16x8_t (&qf)[8], int wave, int32_t t) {
+__device__ __forceinline__ void step(Acc& a, Walk& w, const bf16x8_t (&qf)[8], int wave, int32_t t) {
   if (t > w.n) return;
   constexpr int kLoadSlot = (kSlot + kAhead) % kStages;
   m_phase(a, kSlot, qf, w);
@@ -324,7 +341,7 @@ __device__ __forceinline__ void step(Acc& a, const Walk& w, const bf16x8_t (&qf)
 // 1: offsets given in a.m_off; 2: exact row max only (a.mx).  Accumulates O^T and the row
 // sums from zero (modes 0 and 1).
 template <int kMode, bool kOneRun>
-__device__ __forceinline__ void walk(Acc& a, const Walk& w, const bf16x8_t (&qf)[8], int wave, int group) {
+__device__ __forceinline__ void walk(Acc& a, Walk& w, const bf16x8_t (&qf)[8], int wave, int group) {
   const f32x16_t zero = {};
 #pragma unroll
   for (int d = 0; d < 4; ++d) a.o[d] = zero;
@@ -339,6 +356,11 @@ __device__ __forceinline__ void walk(Acc& a, const Walk& w, const bf16x8_t (&qf)
   // below counts only this walk's stage loads
   __builtin_amdgcn_s_waitcnt(0);
   barrier();                                   // the ring is free
+  if (!kOneRun) {                              // loader cursors at the range's first key
+    w.kc_lo = w.vc_lo = w.seg.run_start(w.k_begin);
+    w.kc_hi = w.vc_hi = min(w.seg.run_end(w.k_begin), w.k_end);
+    w.kc_delta = w.vc_delta = w.seg.row(w.k_begin) - w.k_begin;
+  }
 #pragma unroll
   for (int t = 0; t < kAhead; ++t)
     if (t <= w.n) load_stage<kOneRun>(t, w, wave, t);
