@@ -31,10 +31,11 @@
 // the other wave's MFMAs to drain.
 //
 // Schedule: the (query tile, key tile) units of the launch are cut into `groups` equal
-// contiguous ranges, one per work-group (a balanced split keeps all compute units busy
-// when the query tiles alone would leave some idle).  A query tile whose key range falls
-// to several work-groups gets a normalised partial output and its (offset, row sum) from
-// each, and attn_combine merges them by log-sum-exp.  Work-groups are numbered so that
+// contiguous ranges, one per work-group: either one work-group per query tile (its whole key
+// range), or one per compute unit when the query tiles alone would leave too many idle
+// (attn_plan weighs the two with costs measured on the chip).  A query tile whose key range
+// falls to several work-groups gets a normalised partial output and its (offset, row sum)
+// from each, and attn_combine merges them by log-sum-exp.  Work-groups are numbered so that
 // neighbouring ranges (same head, neighbouring query tiles) land on the same XCD and share
 // its L2 while they stream the same keys.
 #include <hip/hip_runtime.h>
@@ -255,7 +256,10 @@ struct MJob {
   }
 };
 
-__device__ __forceinline__ void m_phase_full(Acc& a, int slot, const bf16x8_t (&qf)[8], const Walk& w) {
+// Every M phase runs all 32 jobs, so the loop has a single path for the accumulators: in
+// the first tile's phase P is still zero (the PV product adds nothing), and in the phase
+// after the last tile the QK product of the duplicate K tile is not used.
+__device__ __forceinline__ void m_phase(Acc& a, int slot, const bf16x8_t (&qf)[8], const Walk& w) {
   bf16x8_t f[32];
 #pragma unroll
   for (int j = 0; j < kFetchAhead; ++j) f[j] = fetch_job(j, slot, w);
@@ -263,12 +267,6 @@ __device__ __forceinline__ void m_phase_full(Acc& a, int slot, const bf16x8_t (&
   MJob<0>::run(a, f, slot, qf, w);
 }
 
-// Every M phase runs all 32 jobs, so the loop has a single path for the accumulators: in
-// the first tile's phase P is still zero (the PV product adds nothing), and in the phase
-// after the last tile the QK product of the duplicate K tile is not used.
-__device__ __forceinline__ void m_phase(Acc& a, int slot, const bf16x8_t (&qf)[8], const Walk& w) {
-  m_phase_full(a, slot, qf, w);
-}
 
 // V phase of tile t: mask keys past the range (last tile), the exponent offsets (first
 // tile of pass 0), then P and its row sums (kMode 2: only the row max), with this wave's

@@ -291,3 +291,24 @@ def test_svd_and_linear_argument_errors():
     assert g(p[0], p[1], None, p[2], 4, 12, 8, None) == u.E_SHAPE
     assert g(p[0], p[1], p[3] + 2, p[2], 4, 8, 8, None) == u.E_ALIGN
     assert u.vo_rank(1536) == 1413
+
+
+def test_schedule_choice_follows_the_measured_costs():
+    # the attention plan (host arithmetic only): one work-group per query tile where the
+    # balanced split over 256 compute units does not pay for its merge and its slower units
+    # (the full-frame chunk, the paper's nine- and eight-frame windows, every call of a 5 s
+    # clip), the balanced split where query tiles alone would leave many units idle (the
+    # unwindowed 32,760-key call, one-frame rolling chunks)
+    def ws(S, R, f0, C, W):
+        rc, h = _handle(1, 12, 30, 52, S, R)
+        assert rc == u.OK
+        b = ctypes.c_size_t(123)
+        assert u.lib.unstep_attn_workspace_size(h, f0, C, W, ctypes.byref(b)) == u.OK
+        u.lib.unstep_cache_destroy(h)
+        return b.value
+    assert ws(0, 12, 9, 3, 9) == 0                 # full-frame chunk, 18,720 keys
+    assert ws(3, 6, 9, 3, 3) == 0                  # nine frames, 14,040 keys
+    assert ws(2, 6, 9, 3, 3) == 0                  # eight frames
+    assert ws(3, 6, 3, 3, 3) == 0                  # second chunk of a clip, six frames
+    assert ws(0, 21, 18, 3, 18) > 0                # unwindowed, 32,760 keys
+    assert ws(0, 12, 20, 1, 11) > 0                # one-frame chunk over 12 frames
