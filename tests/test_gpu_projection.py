@@ -90,6 +90,7 @@ def _linear_bound(x_bits, w_bits, b_bits):
 
 
 @pytest.mark.parametrize("M,N,K,bias", [(4680, 1536, 1536, True), (72, 1536, 1536, True), (4680, 1536, 1536, False),
+                                        (1, 128, 200, True), (300, 256, 8, False), (513, 384, 1032, True),
                                         (1, 40, 48, True), (257, 24, 64, False)])
 def test_linear(M, N, K, bias):
     log(f"linear: M {M} N {N} K {K} bias {bias}")
