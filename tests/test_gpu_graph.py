@@ -1,0 +1,74 @@
+"""The chunk step captured in a HIP graph and replayed: the step path allocates nothing and
+never synchronises, so one capture of unstep_step (append + attention, and the merge of the
+balanced schedule) can be replayed for every denoising call of a chunk, new inputs written into
+its buffers between replays (re-appending a stored frame overwrites it in place, as repeated
+calls do).  Every replay is checked against an eager twin cache bit for bit and against the
+oracle within the stated tolerance.  Inputs from synth only; expected values from oracle only."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import rope, tables
+from tests.gpu_helpers import Mirror, check_attention, dev, host, log, sample_queries
+
+pytestmark = pytest.mark.gpu
+
+u = pytest.importorskip("paper_2609_32518_amd")
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+H, GH, GW, S, R = 2, 30, 52, 0, 12
+C, F0, W = 1, 11, 11          # a one-frame chunk over 11 prior frames: 18,720 keys, balanced schedule
+
+
+def _prefill(m, seed):
+    for f in range(F0):
+        m.append(f, 1, (seed, f))
+
+
+def test_step_replayed_from_a_graph():
+    a = Mirror(u, 1, H, GH, GW, S, R)           # replayed from the graph
+    b = Mirror(u, 1, H, GH, GW, S, R)           # eager twin
+    for m in (a, b):
+        _prefill(m, 60)
+    N = C * a.T
+    ws_bytes = a.lib.workspace_bytes(F0, C, W)
+    assert ws_bytes > 0, "this shape should take the balanced schedule (three kernels captured)"
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device="cuda")
+    shape = (1, N, H, 128)
+    qs, ks, vs = (torch.zeros(shape, dtype=torch.bfloat16, device="cuda") for _ in range(3))
+    q_rot = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
+    out = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
+    cos_t, sin_t = a.tables.get(F0, C, GH, GW)
+    torch.cuda.synchronize()
+
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        a.lib.unstep_step(F0, C, W, qs, ks, vs, cos_t, sin_t, q_rot=q_rot, out=out, workspace=ws)
+    # capture ran the host side once (frame F0 is recorded) and no kernel
+    assert a.lib.frame_map()[1] == F0
+
+    rows = sample_queries(N, 96, 61)
+    for r in range(3):
+        log(f"graph replay {r}")
+        q, k, v = a.inputs(C, (61, r))
+        qs.copy_(dev(q))
+        ks.copy_(dev(k))
+        vs.copy_(dev(v))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        # eager twin with the same inputs
+        qr_b, out_b, _, q_want = b.step(F0, C, W, (61, r))
+        torch.cuda.synchronize()
+        assert torch.equal(q_rot.view(torch.int16), qr_b.view(torch.int16)), f"replay {r}: q_rot"
+        assert torch.equal(out.view(torch.int16), out_b.view(torch.int16)), f"replay {r}: attention output"
+        assert torch.equal(a.lib.k.view(torch.int16), b.lib.k.view(torch.int16)), f"replay {r}: K cache"
+        assert torch.equal(a.lib.v.view(torch.int16), b.lib.v.view(torch.int16)), f"replay {r}: V cache"
+        # and the oracle (the mirror of a re-appends the chunk as the replay did)
+        c, sn = tables.rope_tables(F0, C, GH, GW)
+        a.orc.append(F0, C, rope.rope_bf16(k, c, sn), v)
+        a.check_cache(f"replay {r}")
+        assert np.array_equal(host(q_rot), q_want)
+        want, _ = a.expected(q_want, F0, C, W, query_idx=rows)
+        check_attention(host(out)[:, rows], want, f"replay {r}")
