@@ -324,21 +324,31 @@ __device__ __forceinline__ void v_phase(Acc& a, int32_t t, Walk& w, int wave) {
 // for everyone when phase 2t + 2 (group A's M phase of tile t + 1) starts.  The slot
 // refilled with stage t + 3 (group A in phase 2t + 1, group B in 2t + 2) last held stage
 // t - 1, read by group B in global phase 2t - 1.
-template <int kMode, int kSlot, bool kOneRun>
+template <int kMode, int kSlot, bool kOneRun, bool kIdle>
 __device__ __forceinline__ void step(Acc& a, Walk& w, const bf16x8_t (&qf)[8], int wave, int32_t t) {
   if (t > w.n) return;
   constexpr int kLoadSlot = (kSlot + kAhead) % kStages;
-  m_phase(a, kSlot, qf, w);
+  if (!kIdle) m_phase(a, kSlot, qf, w);
   if (t + 1 <= w.n) wait_stages_in_flight(min(kAhead - 2, w.n - t - 1));
   barrier();
-  if (t < w.n) v_phase<kMode, kLoadSlot, kOneRun>(a, t, w, wave);
+  if (kIdle) {
+    // a wave with no query of the tile: only its share of the loads, in the same order
+    if (t < w.n && t + kAhead <= w.n) {
+      load_rows<kOneRun>(w.lds_k + kLoadSlot * kTileBytes, w.kbase, w, w.kc_lo, w.kc_hi, w.kc_delta, wave,
+                         w.k_begin + min(t + kAhead, w.n - 1) * kBlockK);
+      load_rows<kOneRun>(w.lds_v + kLoadSlot * kTileBytes, w.vbase, w, w.vc_lo, w.vc_hi, w.vc_delta, wave,
+                         w.k_begin + (t + kAhead - 1) * kBlockK);
+    }
+  } else if (t < w.n) {
+    v_phase<kMode, kLoadSlot, kOneRun>(a, t, w, wave);
+  }
   barrier();
 }
 
 // One walk over the key range.  kMode 0: exponent offsets from the first tile (pass 0);
 // 1: offsets given in a.m_off; 2: exact row max only (a.mx).  Accumulates O^T and the row
 // sums from zero (modes 0 and 1).
-template <int kMode, bool kOneRun>
+template <int kMode, bool kOneRun, bool kIdle>
 __device__ __forceinline__ void walk(Acc& a, Walk& w, const bf16x8_t (&qf)[8], int wave, int group) {
   const f32x16_t zero = {};
 #pragma unroll
@@ -366,10 +376,10 @@ __device__ __forceinline__ void walk(Acc& a, Walk& w, const bf16x8_t (&qf)[8], i
   barrier();                                   // stage 0 is complete: global phase 0
   if (group == 1) barrier();                   // group B idles in phase 0
   for (int32_t t0 = 0; t0 <= w.n; t0 += kStages) {
-    step<kMode, 0, kOneRun>(a, w, qf, wave, t0);
-    step<kMode, 1, kOneRun>(a, w, qf, wave, t0 + 1);
-    step<kMode, 2, kOneRun>(a, w, qf, wave, t0 + 2);
-    step<kMode, 3, kOneRun>(a, w, qf, wave, t0 + 3);
+    step<kMode, 0, kOneRun, kIdle>(a, w, qf, wave, t0);
+    step<kMode, 1, kOneRun, kIdle>(a, w, qf, wave, t0 + 1);
+    step<kMode, 2, kOneRun, kIdle>(a, w, qf, wave, t0 + 2);
+    step<kMode, 3, kOneRun, kIdle>(a, w, qf, wave, t0 + 3);
   }
   if (group == 0) barrier();                   // group A idles in the last phase
 }
@@ -490,19 +500,38 @@ __global__ __launch_bounds__(kThreads) void window_attn_kernel(AttnArgs a) {
     Acc acc;
     acc.m_off = 0.f;
     // a range inside the first run of the segment table takes the loader's branch-free path
+    // a wave whose 32 queries all lie past the chunk's end (the last, ragged query tile) runs
+    // the walk's loads and barriers only
+    const bool idle = qt * kBlockQ + wave * 32 >= N;
     if (w.k_end <= w.seg.l1) {
-      walk<0, true>(acc, w, qf, wave, group);
+      if (idle)
+        walk<0, true, true>(acc, w, qf, wave, group);
+      else
+        walk<0, true, false>(acc, w, qf, wave, group);
       if (__syncthreads_or(!(acc.l <= 0x1p64f))) {
-        walk<2, true>(acc, w, qf, wave, group);
-        acc.m_off = fmaxf(acc.mx, __shfl_xor(acc.mx, 32));
-        walk<1, true>(acc, w, qf, wave, group);
+        if (idle) {
+          walk<2, true, true>(acc, w, qf, wave, group);
+          walk<1, true, true>(acc, w, qf, wave, group);
+        } else {
+          walk<2, true, false>(acc, w, qf, wave, group);
+          acc.m_off = fmaxf(acc.mx, __shfl_xor(acc.mx, 32));
+          walk<1, true, false>(acc, w, qf, wave, group);
+        }
       }
     } else {
-      walk<0, false>(acc, w, qf, wave, group);
+      if (idle)
+        walk<0, false, true>(acc, w, qf, wave, group);
+      else
+        walk<0, false, false>(acc, w, qf, wave, group);
       if (__syncthreads_or(!(acc.l <= 0x1p64f))) {
-        walk<2, false>(acc, w, qf, wave, group);
-        acc.m_off = fmaxf(acc.mx, __shfl_xor(acc.mx, 32));
-        walk<1, false>(acc, w, qf, wave, group);
+        if (idle) {
+          walk<2, false, true>(acc, w, qf, wave, group);
+          walk<1, false, true>(acc, w, qf, wave, group);
+        } else {
+          walk<2, false, false>(acc, w, qf, wave, group);
+          acc.m_off = fmaxf(acc.mx, __shfl_xor(acc.mx, 32));
+          walk<1, false, false>(acc, w, qf, wave, group);
+        }
       }
     }
 
