@@ -667,7 +667,16 @@ AttnPlan attn_plan(int32_t B, int32_t H, int32_t N, int32_t n_keys) {
   const size_t ws = attn_workspace_bytes(int32_t(g));
   const double t_bal = double((units + g - 1) / g) * kTileUsBalanced + double(ws) / 4.5e6 + 2.0;
   if (t_bal >= t_plain) return plain;
-  return AttnPlan{int32_t(g), ws, int32_t(qtiles), size_t(g) * 2 * kBlockQ * kHeadDim};
+  // When a whole number of work-groups per query tile nearly fills the chip, split every query
+  // tile into that many equal parts: each work-group then walks one segment (one pipeline
+  // fill, one partial written and merged) instead of the ends of two.  Every work-group keeps
+  // at least 4 units, so none is empty: the merge reads the partial of every work-group between
+  // a tile's first and last owner.
+  const int64_t per = kSlots / qtiles;
+  const int64_t g_aligned = qtiles * per;
+  const int64_t groups = (per >= 2 && g_aligned * 10 >= kSlots * 9 && g_aligned <= units / 4) ? g_aligned : g;
+  const size_t ws_g = attn_workspace_bytes(int32_t(groups));
+  return AttnPlan{int32_t(groups), ws_g, int32_t(qtiles), size_t(groups) * 2 * kBlockQ * kHeadDim};
 }
 
 size_t attn_workspace_bytes(int32_t groups) {

@@ -299,8 +299,8 @@ def test_schedule_choice_follows_the_measured_costs():
     # (the full-frame chunk, the paper's nine- and eight-frame windows, every call of a 5 s
     # clip), the balanced split where query tiles alone would leave many units idle (the
     # unwindowed 32,760-key call, one-frame rolling chunks)
-    def ws(S, R, f0, C, W):
-        rc, h = _handle(1, 12, 30, 52, S, R)
+    def ws(S, R, f0, C, W, H=12, gh=30, gw=52):
+        rc, h = _handle(1, H, gh, gw, S, R)
         assert rc == u.OK
         b = ctypes.c_size_t(123)
         assert u.lib.unstep_attn_workspace_size(h, f0, C, W, ctypes.byref(b)) == u.OK
@@ -312,3 +312,11 @@ def test_schedule_choice_follows_the_measured_costs():
     assert ws(3, 6, 3, 3, 3) == 0                  # second chunk of a clip, six frames
     assert ws(0, 21, 18, 3, 18) > 0                # unwindowed, 32,760 keys
     assert ws(0, 12, 20, 1, 11) > 0                # one-frame chunk over 12 frames
+
+    def part_bytes(groups):                          # two fp32 partials (o, offset, sum) per work-group
+        return groups * 2 * 256 * (128 + 2) * 4
+    # 84 query tiles: 3 work-groups per tile (252 of 256 units), each walks a third of a tile
+    assert ws(0, 12, 20, 1, 11) == part_bytes(252)
+    # 2 query tiles of 400 key tiles: 128 work-groups per tile would get 3 units each, so the
+    # split stays at units / 4 = 200 (no work-group under 4 units, none empty)
+    assert ws(0, 101, 100, 1, 99, H=2, gh=16, gw=16) == part_bytes(200)
