@@ -162,3 +162,27 @@ def sample_queries(N: int, n: int, seed: int) -> np.ndarray:
     rng = np.random.default_rng(seed)
     idx = set(rng.choice(N, size=min(n, N), replace=False).tolist()) | {0, N - 1}
     return np.array(sorted(idx), dtype=np.int64)
+
+
+def random_shape_cases(n_cases: int = 48, seed: int = 2609) -> list:
+    """Seeded small configurations for the randomized parity test: batch 1-2, 1-4 heads, grids
+    up to 8x12 (ragged query and key tiles; the second case has one token per frame), 0-2 sinks (chunks that straddle the
+    sink boundary), chunks of 1-3 frames, windows of 0-9 frames and rings up to 2 frames larger
+    than they need.  Each case carries a call sequence of in-order chunks with repeats of the
+    newest chunk, each call on the balanced or the plain schedule, with or without LSE."""
+    rng = np.random.default_rng([seed, 7])
+    cases = []
+    for i in range(n_cases):
+        B, H = int(rng.integers(1, 3)), int(rng.integers(1, 5))
+        gh, gw = int(rng.integers(1, 9)), int(rng.integers(1, 13))
+        if i == 1:
+            gh = gw = 1                                     # one token per frame
+        S, C, W = int(rng.integers(0, 3)), int(rng.integers(1, 4)), int(rng.integers(0, 10))
+        R = W + C + int(rng.integers(0, 3))
+        calls, f0 = [], 0
+        for _ in range(int(rng.integers(6, 12))):
+            calls.append((f0, bool(rng.integers(0, 4) > 0), bool(rng.integers(0, 2))))
+            if rng.random() < 0.75:
+                f0 += C
+        cases.append(dict(B=B, H=H, gh=gh, gw=gw, S=S, R=R, C=C, W=W, calls=calls))
+    return cases

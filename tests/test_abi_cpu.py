@@ -320,3 +320,35 @@ def test_schedule_choice_follows_the_measured_costs():
     # 2 query tiles of 400 key tiles: 128 work-groups per tile would get 3 units each, so the
     # split stays at units / 4 = 200 (no work-group under 4 units, none empty)
     assert ws(0, 101, 100, 1, 99, H=2, gh=16, gw=16) == part_bytes(200)
+
+
+def test_random_shape_cases_are_valid_and_reach_both_schedules():
+    # the call sequences of the randomized GPU parity test, replayed on the host index and the
+    # oracle's cache model: every call is accepted by both with equal segments, and the cases
+    # reach the balanced schedule, the plain one, chunks across the sink boundary and single tokens
+    from tests.gpu_helpers import random_shape_cases
+    balanced = plain = straddle = 0
+    cases = random_shape_cases()
+    for cs in cases:
+        rc, h = _handle(cs["B"], cs["H"], cs["gh"], cs["gw"], cs["S"], cs["R"])
+        assert rc == u.OK
+        orc = KVCacheOracle(cs["B"], cs["H"], 128, cs["gh"], cs["gw"], cs["S"], cs["R"])
+        C, W = cs["C"], cs["W"]
+        zeros = np.zeros((cs["B"], C * cs["gh"] * cs["gw"], cs["H"], 128), np.uint16)
+        try:
+            for f0, use_split, _ in cs["calls"]:
+                assert u.lib.unstep_cache_advance(h, f0, C) == u.OK
+                orc.append(f0, C, zeros, zeros)
+                rc, segs = _segments(h, f0, C, W)
+                assert rc == u.OK and segs == orc.segments(f0, C, W)
+                b = ctypes.c_size_t()
+                assert u.lib.unstep_attn_workspace_size(h, f0, C, W, ctypes.byref(b)) == u.OK
+                if use_split and b.value > 0:
+                    balanced += 1
+                else:
+                    plain += 1
+                straddle += f0 < cs["S"] < f0 + C
+        finally:
+            u.lib.unstep_cache_destroy(h)
+    assert balanced >= 10 and plain >= 10 and straddle >= 2, (balanced, plain, straddle)
+    assert any(cs["gh"] * cs["gw"] == 1 for cs in cases)

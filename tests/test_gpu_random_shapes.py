@@ -1,0 +1,37 @@
+"""GPU parity over seeded random small shapes (tests/gpu_helpers.random_shape_cases): batch,
+heads, grid, sinks, ring, chunk and window drawn at random, each case a stream of chunk steps
+through unstep_step (repeats of the newest chunk included) on the balanced or the plain
+schedule.  After every call q_rot, both caches and the frame map are bit-exact and the
+attention output (and the log-sum-exp where requested) within the stated tolerance of the
+oracle.  Inputs from synth only; expected values from oracle only."""
+import numpy as np
+import pytest
+import torch
+
+from tests.gpu_helpers import LSE_ABS, Mirror, check_attention, host, log, random_shape_cases
+
+pytestmark = pytest.mark.gpu
+
+u = pytest.importorskip("paper_2609_32518_amd")
+if not torch.cuda.is_available():
+    pytest.skip("needs a GPU", allow_module_level=True)
+
+CASES = random_shape_cases()
+
+
+@pytest.mark.parametrize("case", range(len(CASES)))
+def test_random_shape_stream(case):
+    cs = CASES[case]
+    C, W = cs["C"], cs["W"]
+    log(f"random shape {case}: " + " ".join(f"{k}={v}" for k, v in cs.items() if k != "calls"))
+    m = Mirror(u, cs["B"], cs["H"], cs["gh"], cs["gw"], cs["S"], cs["R"])
+    for n, (f0, use_split, with_lse) in enumerate(cs["calls"]):
+        what = f"case {case} call {n} (f0 {f0}, split {use_split})"
+        q_rot, out, lse, q_ref = m.step(f0, C, W, (5000 + case, n), use_split=use_split, lse=with_lse)
+        torch.cuda.synchronize()
+        assert np.array_equal(host(q_rot), q_ref), f"{what}: q_rot"
+        m.check_cache(what)
+        want, want_lse = m.expected(q_ref, f0, C, W)
+        check_attention(host(out), want, what)
+        if with_lse:
+            assert np.max(np.abs(lse.cpu().numpy() - want_lse)) <= LSE_ABS, f"{what}: lse"
