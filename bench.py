@@ -689,7 +689,7 @@ def main():
         summarize_clip_profile(args.summarize_clip_profile, args)
         return
     if args.gpus != 1:
-        print(f"bench.py: this build measures one GPU only (the step shards by head across GPUs, but no "
+        print(f"bench.py: the library runs on one GPU only (the step shards by head across GPUs, but no "
               f"multi-GPU path is built); got --gpus {args.gpus}", file=sys.stderr)
         sys.exit(2)
     import torch
