@@ -12,9 +12,10 @@ fallback path.  Build it with ``python paper_2609_32518_amd/build.py``.
 """
 from __future__ import annotations
 
+import collections
 import ctypes
 import os
-from typing import Dict, List, Optional, Tuple
+from typing import List, Optional, Tuple
 
 import torch
 
@@ -118,17 +119,30 @@ def unstep_rope_tables(start_frame: int, n_frames: int, grid_h: int, grid_w: int
 
 class RopeTableCache:
     """Tables keyed by (start frame, n_frames, grid_h, grid_w, theta), built once and reused
-    by every layer and denoising call of that chunk (Appendix A.5)."""
+    by every layer and denoising call of that chunk (Appendix A.5).  At most `max_entries`
+    pairs are kept, the least recently used dropped first, so an endless stream of chunks
+    holds a bounded amount of device memory (a dropped pair is rebuilt if asked for again;
+    kernels already queued on the stream keep its memory until they have run)."""
 
-    def __init__(self, device="cuda"):
+    def __init__(self, device="cuda", max_entries: int = 64):
+        if max_entries < 1:
+            raise ValueError("max_entries must be >= 1")
         self.device = device
-        self._tables: Dict[tuple, Tuple[torch.Tensor, torch.Tensor]] = {}
+        self.max_entries = max_entries
+        self._tables: "collections.OrderedDict[tuple, Tuple[torch.Tensor, torch.Tensor]]" = collections.OrderedDict()
+
+    def __len__(self) -> int:
+        return len(self._tables)
 
     def get(self, start_frame: int, n_frames: int, grid_h: int, grid_w: int, theta: float = 10000.0):
         key = (start_frame, n_frames, grid_h, grid_w, theta)
-        if key not in self._tables:
+        if key in self._tables:
+            self._tables.move_to_end(key)
+        else:
             self._tables[key] = unstep_rope_tables(start_frame, n_frames, grid_h, grid_w, HEAD_DIM, theta,
                                                    self.device)
+            while len(self._tables) > self.max_entries:
+                self._tables.popitem(last=False)
         return self._tables[key]
 
 

@@ -120,3 +120,20 @@ def test_maximum_cache_with_wrapped_ring():
     assert np.abs(got - want[None, :]).max() <= 2.0 ** -8 * 3.0 + 1e-3
     want_lse = math.log(math.exp(a) + n_keys - 1)
     assert np.abs(lse.cpu().numpy() - want_lse).max() <= 1e-3
+
+
+def test_rope_table_cache_is_bounded():
+    # least recently used pairs are dropped beyond max_entries and rebuilt identically on demand
+    from oracle import tables as otables
+    cache = u.RopeTableCache("cuda", max_entries=2)
+    a = cache.get(0, 3, 4, 6)
+    cache.get(3, 3, 4, 6)
+    assert cache.get(0, 3, 4, 6) is a                # a hit refreshes the pair
+    cache.get(6, 3, 4, 6)                            # drops (3, 3, ...), the least recently used
+    assert len(cache) == 2 and cache.get(0, 3, 4, 6) is a
+    c, s = cache.get(3, 3, 4, 6)                     # rebuilt
+    torch.cuda.synchronize()
+    oc, os_ = otables.rope_tables(3, 3, 4, 6)
+    assert np.array_equal(c.cpu().numpy().view(np.uint32), oc.view(np.uint32))
+    assert np.array_equal(s.cpu().numpy().view(np.uint32), os_.view(np.uint32))
+    assert len(cache) == 2
