@@ -292,9 +292,11 @@ int unstep_svd_truncate(const float* w, int32_t rows, int32_t cols, int32_t rank
  * [N, K] (the nn.Linear layout [out, in]), bias bf16 [N] or NULL, y bf16 [M, N]; all
  * row-major and contiguous, on the device.  float32 accumulation and bias add, bf16 result
  * (a plain GEMM with a bias epilogue, run by hipBLASLt on hip_stream).  The first call on a
- * device creates the GEMM library's handle and a 32 MB device workspace (kept until the
- * process ends); the first call for a shape times the library's candidate algorithms on its
- * own operands, synchronising the stream once, and keeps the fastest.
+ * device creates the GEMM library's handle, and the first call on each (device, stream) a
+ * 32 MB device workspace of its own, so calls on different streams may overlap (both kept
+ * until the process ends); the first call for a shape times the library's candidate
+ * algorithms on its own operands, synchronising the stream once, and keeps the fastest.
+ * Calls from several host threads are serialised inside the library.
  * Errors: E_NULL (x, w, y), E_SHAPE (sizes < 1, K or N not a multiple of 8, no algorithm for
  * the shape), E_ALIGN, E_HIP. */
 int unstep_linear(const void* x, const void* w, const void* bias, void* y, int32_t M, int32_t N, int32_t K,

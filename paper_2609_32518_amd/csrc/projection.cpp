@@ -30,6 +30,7 @@
 #include <map>
 #include <mutex>
 #include <tuple>
+#include <utility>
 #include <vector>
 
 #include "kernels.hpp"
@@ -78,14 +79,17 @@ hipblasLtHandle_t lt_handle(int dev) {
 constexpr size_t kLinearWorkspace = size_t(32) << 20;   // per device, for algorithms that want it
 constexpr int kCandidates = 16;
 
-// Device scratch of the GEMM library, allocated once per device (first call).
-void* lt_workspace(int dev) {
-  static std::map<int, void*> ws;
-  auto it = ws.find(dev);
+// Device scratch of the GEMM library, one per (device, stream), allocated on the first call
+// that uses the pair: GEMMs enqueued on different streams may run at the same time, so they
+// must not share scratch; calls on one stream run in order and do.
+void* lt_workspace(int dev, hipStream_t st) {
+  static std::map<std::pair<int, hipStream_t>, void*> ws;
+  const auto key = std::make_pair(dev, st);
+  auto it = ws.find(key);
   if (it != ws.end()) return it->second;
   void* p = nullptr;
   if (hipMalloc(&p, kLinearWorkspace) != hipSuccess) return nullptr;
-  ws[dev] = p;
+  ws[key] = p;
   return p;
 }
 
@@ -98,7 +102,7 @@ const LinearPlan* linear_plan(int dev, int32_t M, int32_t N, int32_t K, const vo
                               int* rc) {
   static std::map<std::tuple<int, int32_t, int32_t, int32_t, bool>, LinearPlan> plans;
   hipblasLtHandle_t h = lt_handle(dev);
-  void* ws = lt_workspace(dev);
+  void* ws = lt_workspace(dev, st);
   *h_out = h;
   *ws_out = ws;
   if (!h || !ws) {

@@ -105,3 +105,33 @@ def test_linear(M, N, K, bias):
     lim = 2.0 ** -8 * np.abs(want) + _linear_bound(x, w, b)
     log(f"  max err {err.max():.3g}, mean err {err.mean():.3g}; worst slack {(err / lim).max():.3f}")
     assert np.all(err <= lim)
+
+
+@pytest.mark.parametrize("M,N,K", [(4680, 1536, 1536), (64, 1536, 12288)])
+def test_linear_on_two_streams_at_once(M, N, K):
+    # calls enqueued on two streams may run at the same time: each stream has its own GEMM
+    # scratch, so every result stays within the oracle's bound (a shared scratch would mix the
+    # two products); the deep-K shape is one where split-K algorithms, which use scratch, are
+    # candidates
+    log(f"linear on two streams: M {M} N {N} K {K}")
+    xs = [dev(synth.normal_bf16((M, K), (M, N, K, 10 + i))) for i in range(2)]
+    w = dev(synth.normal_bf16((N, K), (M, N, K, 12), 1.0 / np.sqrt(K)))
+    b = dev(synth.normal_bf16((N,), (M, N, K, 13)))
+    alone = [u.unstep_linear(x, w, b) for x in xs]                # plan chosen here, default stream
+    torch.cuda.synchronize()
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    outs = [[torch.empty((M, N), dtype=torch.bfloat16, device="cuda") for _ in range(4)] for _ in range(2)]
+    torch.cuda.synchronize()
+    for rep in range(4):
+        for i in range(2):
+            u.unstep_linear(xs[i], w, b, out=outs[i][rep], stream=streams[i])
+    torch.cuda.synchronize()
+    for i in range(2):
+        want = svd.linear(host(xs[i]), host(w), host(b))
+        lim = 2.0 ** -8 * np.abs(want) + _linear_bound(host(xs[i]), host(w), host(b))
+        same = 0
+        for rep in range(4):
+            got = numerics.bf16_to_f64(host(outs[i][rep]))
+            assert np.all(np.abs(got - want) <= lim), (i, rep)
+            same += bool(torch.equal(outs[i][rep].view(torch.int16), alone[i].view(torch.int16)))
+        log(f"  stream {i}: {same} of 4 results bit-identical to the call run alone")
