@@ -25,7 +25,10 @@
  *   - Every function returns UNSTEP_OK or a negative unstep_status and never aborts;
  *     unstep_last_error() then describes the failure.  All argument and state checks
  *     happen before any work is enqueued; a failed call changes no state.
- *   - A cache handle is not thread-safe; distinct handles are independent.
+ *   - A cache handle is not thread-safe; distinct handles are independent.  Calls on one
+ *     handle must also run in order on the device (one stream, or events between streams):
+ *     each reads the cache rows the previous ones wrote.  An attention workspace must not be
+ *     in use by another call that may run at the same time.
  *   - Only head_dim == 128 is supported (the model's 12 heads of width 128, App. A.5).
  */
 #ifndef UNSTEP_H

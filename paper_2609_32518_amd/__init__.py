@@ -90,6 +90,17 @@ def _stream(stream: Optional[torch.cuda.Stream]) -> int:
     return s.cuda_stream
 
 
+def _used_on(stream: Optional[torch.cuda.Stream], *tensors: Optional[torch.Tensor]) -> None:
+    """Tell torch's allocator that work enqueued on `stream` uses these tensors, so that their
+    memory is not handed to a new allocation before that work has run.  Needed when `stream`
+    is not the current stream, on which the wrappers allocate outputs and scratch."""
+    if stream is None or stream == torch.cuda.current_stream():
+        return
+    for t in tensors:
+        if t is not None:
+            t.record_stream(stream)
+
+
 def version() -> int:
     return lib.unstep_version()
 
@@ -114,6 +125,7 @@ def unstep_rope_tables(start_frame: int, n_frames: int, grid_h: int, grid_w: int
     s = torch.empty_like(c)
     _check(lib.unstep_rope_tables(start_frame, n_frames, grid_h, grid_w, head_dim, theta, c.data_ptr(),
                                   s.data_ptr(), _stream(stream)))
+    _used_on(stream, c, s)
     return c, s
 
 
@@ -223,6 +235,7 @@ class Cache:
                                 device=k.device)
         _check(lib.unstep_kv_append(self.handle, start_frame, n_frames, _ptr(q), k.data_ptr(), v.data_ptr(), ts, hs,
                                     cos_t.data_ptr(), sin_t.data_ptr(), _ptr(q_rot), _stream(stream)))
+        _used_on(stream, q_rot)
         return q_rot
 
     def unstep_kv_append_qknorm(self, start_frame: int, n_frames: int, q: Optional[torch.Tensor], k: torch.Tensor,
@@ -244,6 +257,7 @@ class Cache:
         _check(lib.unstep_kv_append_qknorm(self.handle, start_frame, n_frames, _ptr(q), k.data_ptr(), v.data_ptr(),
                                            ts, hs, cos_t.data_ptr(), sin_t.data_ptr(), _ptr(q_norm_weight),
                                            k_norm_weight.data_ptr(), norm_eps, _ptr(q_rot), _stream(stream)))
+        _used_on(stream, q_rot)
         return q_rot
 
     def unstep_window_attn(self, start_frame: int, n_frames: int, window_frames: int, q_rot: torch.Tensor,
@@ -258,6 +272,7 @@ class Cache:
         _check(lib.unstep_window_attn(self.handle, start_frame, n_frames, window_frames, q_rot.data_ptr(),
                                       out.data_ptr(), _ptr(lse), softmax_scale, _ptr(workspace), ws_bytes,
                                       _stream(stream)))
+        _used_on(stream, out, workspace)
         return out
 
     def unstep_step(self, start_frame: int, n_frames: int, window_frames: int, q: torch.Tensor, k: torch.Tensor,
@@ -280,6 +295,7 @@ class Cache:
                                v.data_ptr(), ts, hs, cos_t.data_ptr(), sin_t.data_ptr(), q_rot.data_ptr(),
                                out.data_ptr(), _ptr(lse), softmax_scale, _ptr(workspace), ws_bytes,
                                _stream(stream)))
+        _used_on(stream, q_rot, out, workspace)
         return out
 
     def _step_workspace(self, start_frame: int, n_frames: int, window_frames: int) -> Optional[torch.Tensor]:
@@ -332,6 +348,7 @@ def unstep_linear(x: torch.Tensor, w: torch.Tensor, bias: Optional[torch.Tensor]
     if out is None:
         out = torch.empty(x.shape[:-1] + (N,), dtype=torch.bfloat16, device=x.device)
     _check(lib.unstep_linear(x.data_ptr(), w.data_ptr(), _ptr(bias), out.data_ptr(), M, N, K, _stream(stream)))
+    _used_on(stream, out)
     return out
 
 
@@ -377,6 +394,7 @@ def unstep_renoise(x: torch.Tensor, eps: torch.Tensor, sigma: float, out: Option
     out = torch.empty_like(x) if out is None else out
     _latent(out)
     _check(lib.unstep_renoise(x.data_ptr(), eps.data_ptr(), sigma, out.data_ptr(), x.numel(), _stream(stream)))
+    _used_on(stream, out)
     return out
 
 
@@ -390,4 +408,5 @@ def unstep_emit(x_tilde: torch.Tensor, v: torch.Tensor, sigma: float, out: Optio
     out = torch.empty_like(x_tilde) if out is None else out
     _latent(out)
     _check(lib.unstep_emit(x_tilde.data_ptr(), v.data_ptr(), sigma, out.data_ptr(), x_tilde.numel(), _stream(stream)))
+    _used_on(stream, out)
     return out

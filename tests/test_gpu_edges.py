@@ -10,9 +10,10 @@ import numpy as np
 import pytest
 import torch
 
-from oracle import numerics
+from oracle import numerics, rope
+from oracle import tables as otables
 from oracle.kvcache import KVCacheOracle, retained_frames, slot_of_frame
-from tests.gpu_helpers import Mirror, check_attention, host, log
+from tests.gpu_helpers import Mirror, check_attention, dev, host, log
 
 pytestmark = pytest.mark.gpu
 
@@ -124,7 +125,6 @@ def test_maximum_cache_with_wrapped_ring():
 
 def test_rope_table_cache_is_bounded():
     # least recently used pairs are dropped beyond max_entries and rebuilt identically on demand
-    from oracle import tables as otables
     cache = u.RopeTableCache("cuda", max_entries=2)
     a = cache.get(0, 3, 4, 6)
     cache.get(3, 3, 4, 6)
@@ -137,3 +137,27 @@ def test_rope_table_cache_is_bounded():
     assert np.array_equal(c.cpu().numpy().view(np.uint32), oc.view(np.uint32))
     assert np.array_equal(s.cpu().numpy().view(np.uint32), os_.view(np.uint32))
     assert len(cache) == 2
+
+
+def test_step_on_a_side_stream_with_wrapper_allocations():
+    # the binding allocates q_rot, out and the split-key scratch itself and the work runs on a
+    # stream other than the current one (the scratch grows from plain to balanced shapes on the
+    # way); results as on the current stream, checked against the oracle
+    m = Mirror(u, 1, 2, 30, 52, 0, 12)
+    side = torch.cuda.Stream()
+    for f0 in range(0, 11):
+        m.append(f0, 1, (42, f0))
+    torch.cuda.synchronize()
+    for n, (f0, W) in enumerate([(11, 0), (11, 11), (11, 11)]):
+        q, k, v = m.inputs(1, (43, n))
+        cos_t, sin_t = m.tables.get(f0, 1, 30, 52)
+        qd, kd, vd = dev(q), dev(k), dev(v)
+        side.wait_stream(torch.cuda.current_stream())
+        out = m.lib.unstep_step(f0, 1, W, qd, kd, vd, cos_t, sin_t, stream=side)
+        side.synchronize()
+        c, s = otables.rope_tables(f0, 1, 30, 52)
+        m.orc.append(f0, 1, rope.rope_bf16(k, c, s), v)
+        m.check_cache(f"side stream call {n}")
+        want, _ = m.expected(rope.rope_bf16(q, c, s), f0, 1, W)
+        check_attention(host(out), want, f"side stream call {n}")
+        del out
