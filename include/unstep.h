@@ -76,7 +76,8 @@ typedef struct unstep_cache unstep_cache;
  * caller keeps alive until unstep_cache_destroy.  The handle starts empty (no frame
  * stored).  Touches no device memory.  Errors: E_NULL (out, k_cache, v_cache),
  * E_SHAPE (head_dim != 128, batch/n_heads/grid < 1, sink_frames < 0, ring_frames < 1,
- * more than 2^31 bytes per (batch, head) cache, i.e. (S + R) * T > 8388607 rows),
+ * more than 2^31 bytes per (batch, head) cache, i.e. (S + R) * T > 8388607 rows,
+ * batch * n_heads > 65535, or T * n_heads > 134217727 tokens x heads per frame),
  * E_ALIGN. */
 int unstep_cache_create(unstep_cache** out, int32_t batch, int32_t n_heads, int32_t head_dim,
                         int32_t grid_h, int32_t grid_w, int32_t sink_frames, int32_t ring_frames,

@@ -160,8 +160,10 @@ int unstep_cache_create(unstep_cache** out, int32_t batch, int32_t n_heads, int3
     return fail(UNSTEP_E_SHAPE, "unstep_cache_create: sizes must be >= 1 (sink_frames >= 0)");
   const int64_t T = int64_t(grid_h) * grid_w;
   const int64_t slots = (int64_t(sink_frames) + ring_frames) * T;
-  // kernels address one (batch, head)'s rows with 32-bit byte offsets (rows x 256 B)
-  if (slots * UNSTEP_HEAD_DIM * 2 > INT32_MAX || int64_t(batch) * n_heads > 65535 || T > INT32_MAX / 64)
+  // kernels address one (batch, head)'s rows with 32-bit byte offsets (rows x 256 B), and the
+  // append pass numbers the 16-byte pieces of one frame's tokens x heads in 32 bits
+  if (slots * UNSTEP_HEAD_DIM * 2 > INT32_MAX || int64_t(batch) * n_heads > 65535 || T > INT32_MAX / 64 ||
+      T * n_heads * (UNSTEP_HEAD_DIM * 2 / 16) > INT32_MAX)
     return fail(UNSTEP_E_SHAPE, "unstep_cache_create: cache too large");
   if (!aligned16(k_cache) || !aligned16(v_cache))
     return fail(UNSTEP_E_ALIGN, "unstep_cache_create: cache buffers must be 16-byte aligned");

@@ -74,6 +74,14 @@ def test_create_errors():
     assert _handle(1, 2, 2, 3, 0, 0)[0] == u.E_SHAPE
     assert _handle(1, 2, 2, 3, 0, 4, k=0)[0] == u.E_NULL
     assert _handle(1, 2, 2, 3, 0, 4, k=FAKE[0] + 8)[0] == u.E_ALIGN
+    # size limits: 2^31 bytes per (batch, head), 65535 (batch, head) pairs, and the append
+    # pass's 32-bit piece count per frame (T * H * 16)
+    assert _handle(1, 1, 4096, 2048, 0, 1)[0] == u.E_SHAPE                # 2^23 rows
+    assert _handle(256, 256, 1, 1, 0, 1)[0] == u.E_SHAPE
+    assert _handle(1, 64, 2048, 1024, 0, 1)[0] == u.E_SHAPE               # 2^21 tokens x 64 heads
+    rc, h = _handle(1, 63, 2048, 1024, 0, 1)                              # 2^21 x 63 x 16 < 2^31
+    assert rc == u.OK
+    u.lib.unstep_cache_destroy(h)
     assert u.lib.unstep_cache_destroy(None) == u.OK
 
 
