@@ -199,7 +199,8 @@ int unstep_kv_append_qknorm(unstep_cache* c, int32_t start_frame, int32_t n_fram
  * results up to fp32 summation order, possibly slower).  The size depends only on the
  * shapes (batch, heads, chunk tokens, retained key count), not on what is stored, so it
  * can be queried before the chunk is appended.
- * Errors: those of unstep_window_segments, plus E_NULL (q_rot, out), E_ALIGN, E_HIP;
+ * Errors: those of unstep_window_segments, plus E_NULL (q_rot, out), E_SHAPE (batch * heads *
+ * ceil(N / 256) >= 2^23 query tiles), E_ALIGN, E_HIP;
  * unstep_attn_workspace_size: E_NULL, E_SHAPE, E_RANGE (argument checks only). */
 int unstep_attn_workspace_size(const unstep_cache* c, int32_t start_frame, int32_t n_frames,
                                int32_t window_frames, size_t* bytes);

@@ -105,6 +105,9 @@ int plan_attn(const unstep_cache* c, const unstep::CacheIndex& idx, int32_t f0, 
       (workspace && !aligned16(workspace)))
     return fail(UNSTEP_E_ALIGN, "%s: pointers must be 16-byte aligned", where);
   const int32_t N = C * idx.T();
+  // one 512-thread work-group per 256-query tile: the launch's work-item count must fit 32 bits
+  if (int64_t(c->B) * c->H * ((int64_t(N) + 255) / 256) * 512 > int64_t(UINT32_MAX))
+    return fail(UNSTEP_E_SHAPE, "%s: too many query tiles (batch x heads x chunk tokens / 256 >= 2^23)", where);
   a->q = static_cast<const uint16_t*>(q_rot);
   a->k_cache = c->k;
   a->v_cache = c->v;

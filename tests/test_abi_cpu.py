@@ -360,3 +360,20 @@ def test_random_shape_cases_are_valid_and_reach_both_schedules():
             u.lib.unstep_cache_destroy(h)
     assert balanced >= 10 and plain >= 10 and straddle >= 2, (balanced, plain, straddle)
     assert any(cs["gh"] * cs["gw"] == 1 for cs in cases)
+
+
+def test_attention_rejects_more_query_tiles_than_one_launch_holds():
+    # 255 x 256 (batch, head) pairs of 2-frame chunks of 32,768 tokens: 2^24 - 2^16 query tiles
+    # of 256, more 512-thread work-groups than one launch dimension's 32-bit work-item count
+    # holds; rejected before anything is enqueued
+    rc, h = _handle(255, 256, 128, 256, 0, 2)
+    assert rc == u.OK
+    try:
+        assert u.lib.unstep_cache_advance(h, 0, 2) == u.OK
+        p = FAKE
+        assert u.lib.unstep_window_attn(h, 0, 2, 0, p[6], p[7], None, 0.0, None, 0, None) == u.E_SHAPE
+        assert b"query tiles" in u.lib.unstep_last_error()
+        b = ctypes.c_size_t()
+        assert u.lib.unstep_attn_workspace_size(h, 1, 1, 1, ctypes.byref(b)) == u.OK
+    finally:
+        u.lib.unstep_cache_destroy(h)
