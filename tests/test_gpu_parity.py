@@ -76,13 +76,16 @@ def test_unwindowed(u):
     log("unwindowed: chunk@18 W=18 (32760 keys)")
     m = Mirror(u, wl.B, wl.H, wl.grid_h, wl.grid_w, wl.S, wl.R)
     _prefill(m, wl, 3, wl.f0)
-    q_rot, out, _, q_rot_ref = m.step(wl.f0, wl.C, wl.W, (3, 100))
+    # the balanced schedule: the merge kernel writes both the output and the log-sum-exp
+    assert m.lib.workspace_bytes(wl.f0, wl.C, wl.W) > 0
+    q_rot, out, lse, q_rot_ref = m.step(wl.f0, wl.C, wl.W, (3, 100), lse=True)
     torch.cuda.synchronize()
     assert np.array_equal(host(q_rot), q_rot_ref)
     m.check_cache("unwindowed")
     idx = sample_queries(wl.n_query, 128, 8)
-    want, _ = m.expected(q_rot_ref, wl.f0, wl.C, wl.W, query_idx=idx)
+    want, want_lse = m.expected(q_rot_ref, wl.f0, wl.C, wl.W, query_idx=idx)
     log(f"  {check_attention(host(out)[:, idx], want, 'unwindowed')}")
+    assert np.max(np.abs(lse.cpu().numpy()[:, :, idx] - want_lse)) <= LSE_ABS
 
 
 @pytest.mark.parametrize("group", [0, 1, 2])
@@ -113,13 +116,16 @@ def test_rolling_stream_60_chunks(u):
     log("rolling: 60 one-frame chunks through a 12-frame ring")
     m = Mirror(u, wl.B, wl.H, wl.grid_h, wl.grid_w, wl.S, wl.R)
     for c in range(wl.chunks):
-        q_rot, out, _, q_rot_ref = m.step(c, 1, wl.W, (5, c))
+        with_lse = c % 5 == 4          # the equal split of each query tile and its merge, with LSE
+        q_rot, out, lse, q_rot_ref = m.step(c, 1, wl.W, (5, c), lse=with_lse)
         torch.cuda.synchronize()
         assert np.array_equal(host(q_rot), q_rot_ref), c
         m.check_cache(f"rolling chunk {c}")
         idx = sample_queries(wl.n_query, 24, 100 + c)
-        want, _ = m.expected(q_rot_ref, c, 1, wl.W, query_idx=idx)
+        want, want_lse = m.expected(q_rot_ref, c, 1, wl.W, query_idx=idx)
         st = check_attention(host(out)[:, idx], want, f"rolling chunk {c}")
+        if with_lse:
+            assert np.max(np.abs(lse.cpu().numpy()[:, :, idx] - want_lse)) <= LSE_ABS, c
         if c % 15 == 0 or c == wl.chunks - 1:
             log(f"  chunk {c}: keys {min(c + 1, 12) * 1560} {st}")
 
@@ -129,12 +135,13 @@ def test_paper_default_sinks(u):
     log("paper_default: 3 sinks + 6 recent frames (14040 keys)")
     m = Mirror(u, wl.B, wl.H, wl.grid_h, wl.grid_w, wl.S, wl.R)
     _prefill(m, wl, 6, wl.f0)
-    q_rot, out, _, q_rot_ref = m.step(wl.f0, wl.C, wl.W, (6, 100))
+    q_rot, out, lse, q_rot_ref = m.step(wl.f0, wl.C, wl.W, (6, 100), lse=True)
     torch.cuda.synchronize()
     m.check_cache("paper_default")
     assert sum(l for _, l in m.lib.segments(wl.f0, wl.C, wl.W)) == 14040
     idx = sample_queries(wl.n_query, 128, 10)
-    want, _ = m.expected(q_rot_ref, wl.f0, wl.C, wl.W, query_idx=idx)
+    want, want_lse = m.expected(q_rot_ref, wl.f0, wl.C, wl.W, query_idx=idx)
+    assert np.max(np.abs(lse.cpu().numpy()[:, :, idx] - want_lse)) <= LSE_ABS
     log(f"  {check_attention(host(out)[:, idx], want, 'paper_default')}")
 
 
