@@ -30,10 +30,14 @@
 // probabilities with plain fp32 adds: the packed dot-product instructions would wait for
 // the other wave's MFMAs to drain.
 //
+// Waves whose 32 queries all lie past the chunk's end (in the ragged last query tile) run the
+// loads and barriers of the walk only.
+//
 // Schedule: the (query tile, key tile) units of the launch are cut into `groups` equal
 // contiguous ranges, one per work-group: either one work-group per query tile (its whole key
-// range), or one per compute unit when the query tiles alone would leave too many idle
-// (attn_plan weighs the two with costs measured on the chip).  A query tile whose key range
+// range), or about one per compute unit when the query tiles alone would leave too many idle
+// (attn_plan weighs the two with costs measured on the chip); in the second case every query
+// tile is cut into k equal parts when a whole number k >= 2 per tile nearly fills the chip.  A query tile whose key range
 // falls to several work-groups gets a normalised partial output and its (offset, row sum)
 // from each, and attn_combine merges them by log-sum-exp.  Work-groups are numbered so that
 // neighbouring ranges (same head, neighbouring query tiles) land on the same XCD and share
