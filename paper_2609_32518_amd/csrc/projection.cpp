@@ -17,9 +17,9 @@
 // epilogue, run by hipBLASLt.  In column-major terms y^T [N, M] = W [N, K] x^T [K, M]: A = W
 // stored K x N (ld K) with op T, B = x stored K x M (ld K), D = y stored N x M (ld N); the bias
 // runs along D's rows.  Plans (descriptors + chosen algorithm) are cached per device and shape:
-// the first call on a device creates the library handle and a 32 MB workspace, the first call
-// for a shape times hipBLASLt's candidate algorithms on its own operands (synchronising once)
-// and keeps the fastest.
+// the first call on a device creates the library handle, the first call on a (device, stream)
+// a 32 MB workspace of its own, and the first call for a shape times hipBLASLt's candidate
+// algorithms on its own operands (synchronising once) and keeps the fastest.
 #include <hip/hip_runtime.h>
 #include <hipblaslt/hipblaslt.h>
 #include <rocblas/rocblas.h>
