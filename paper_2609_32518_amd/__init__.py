@@ -5,7 +5,9 @@ Argument marshalling only: every step of the path runs in the library's HIP kern
 PyTorch provides device memory (tensors) and the stream; the library's C ABI
 (include/unstep.h) takes raw pointers.  The binding has the same names as the ABI:
 ``unstep_rope_tables``, ``unstep_kv_append`` (+ ``_qknorm``), ``unstep_window_attn``, ``unstep_step``
-as methods/functions below, plus a ``Cache`` handle.
+as methods of a ``Cache`` handle (or functions), ``RopeTableCache`` for the per-chunk tables, and
+the clip-level calls ``unstep_sampler_calls``, ``unstep_shift_schedule``, ``unstep_renoise``,
+``unstep_emit``, ``unstep_svd_truncate`` and ``unstep_linear``.
 
 Importing this package loads libunstep.so and raises if it is missing: there is no
 fallback path.  Build it with ``python paper_2609_32518_amd/build.py``.
