@@ -2,7 +2,9 @@
 key, a zero window with sinks, and a cache at the maximum size the ABI accepts (just under
 2^31 bytes per (batch, head) buffer) whose ring has wrapped, checked against closed forms the
 oracle's cache model gives (every retained key equally weighted; one dominant needle key far
-out in the buffer, which also drives the work-group's exact-max fallback).
+out in the buffer, which also drives the work-group's exact-max fallback).  Also: the bounded
+rotary table cache, the step on a stream other than the current one, and a cache restored
+from a snapshot of its buffers through unstep_cache_advance.
 Inputs from synth or closed-form recipes; expected values from oracle only."""
 import math
 
@@ -161,3 +163,35 @@ def test_step_on_a_side_stream_with_wrapper_allocations():
         want, _ = m.expected(rope.rope_bf16(q, c, s), f0, 1, W)
         check_attention(host(out), want, f"side stream call {n}")
         del out
+
+
+def test_snapshot_restore_through_advance():
+    # the whole cache state is the K/V buffers plus the frame map: copy the buffers of a cache
+    # built by real appends (3 sinks, a ring that has wrapped), record the same frames in a new
+    # handle over the copies with unstep_cache_advance, and the restored cache attends and then
+    # continues the stream exactly as the original
+    m = Mirror(u, 1, 2, 6, 8, 3, 6)
+    for f0 in range(0, 15, 3):
+        m.append(f0, 3, (44, f0))
+    torch.cuda.synchronize()
+    k2, v2 = m.lib.k.clone(), m.lib.v.clone()
+    r = u.Cache(1, 2, 6, 8, 3, 6, k_cache=k2, v_cache=v2)
+    for f0 in range(0, 15, 3):
+        r.advance(f0, 3)
+    assert r.frame_map() == m.lib.frame_map()
+    assert r.segments(12, 3, 3) == m.lib.segments(12, 3, 3)
+    for n in range(2):
+        q, k, v = m.inputs(3, (45, n))
+        cos_t, sin_t = m.tables.get(15 + 3 * n, 3, 6, 8)
+        outs = []
+        for cache in (m.lib, r):
+            outs.append(cache.unstep_step(15 + 3 * n, 3, 3, dev(q), dev(k), dev(v), cos_t, sin_t))
+        torch.cuda.synchronize()
+        assert torch.equal(outs[0].view(torch.int16), outs[1].view(torch.int16)), n
+        assert torch.equal(m.lib.k.view(torch.int16), r.k.view(torch.int16)), n
+        assert torch.equal(m.lib.v.view(torch.int16), r.v.view(torch.int16)), n
+        c, s = otables.rope_tables(15 + 3 * n, 3, 6, 8)
+        m.orc.append(15 + 3 * n, 3, rope.rope_bf16(k, c, s), v)
+        want, _ = m.expected(rope.rope_bf16(q, c, s), 15 + 3 * n, 3, 3)
+        check_attention(host(outs[1]), want, f"restored cache call {n}")
+    m.check_cache("after the restored run")
