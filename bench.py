@@ -76,6 +76,11 @@ def parse():
                    help="read the rocprofv3 CSV output of the profiling commands under DIR (see "
                         "profile_commands()), write profiles/<kernel>_<workload>.md and "
                         "profiles/traffic.json, and exit")
+    p.add_argument("--summarize-trace", metavar="DIR", default=None,
+                   help="write profiles/kernels_<--trace-name>.md from the rocprofv3 --kernel-trace --stats "
+                        "output in DIR (any bench mode; --trace-command is the command that made it)")
+    p.add_argument("--trace-name", default=None)
+    p.add_argument("--trace-command", default=None)
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MB",
                    help="only run a plain device-to-device copy of MB megabytes (x5), for scaling HBM "
                         "byte counters read by a profiler")
@@ -429,6 +434,33 @@ def summarize_profile(d, workload="full_chunk", qknorm=False):
     print("\n".join(lines))
 
 
+def summarize_trace(d, name, command):
+    """A kernel-time summary of one rocprofv3 --kernel-trace --stats run of any bench mode: the
+    stats table and the bench's own JSON line (the last line of the run's log, DIR/run.log)."""
+    import csv
+    import glob
+    stats_files = glob.glob(os.path.join(d, "*_kernel_stats.csv"))
+    if not stats_files:
+        raise SystemExit(f"no *_kernel_stats.csv under {d}")
+    stats = list(csv.DictReader(open(stats_files[0])))
+    lines = [f"# Kernel profile — {name}", "",
+             "Command (repo root, one MI355X, after `cd /tmp && export TMPDIR=/tmp && cd -`; this file was "
+             "written by `python bench.py --summarize-trace DIR --trace-name NAME --trace-command CMD`):", "",
+             "```", command, "```", "", "## rocprofv3 --stats", "",
+             "| kernel | calls | average µs | min µs | max µs | % of GPU time |", "|---|---|---|---|---|---|"]
+    for r in stats[:8]:
+        lines.append(f"| {r['Name'][:90]} | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | {float(r['Percentage']):.1f} |")
+    log = os.path.join(d, "run.log")
+    if os.path.exists(log):
+        last = [ln for ln in open(log).read().splitlines() if ln.startswith("{")]
+        if last:
+            lines += ["", "## The run's bench line", "", "```", last[-1], "```"]
+    out = os.path.join(ROOT, "profiles", f"kernels_{name}.md")
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def summarize_clip_profile(d, args):
     """Per-call breakdown of the last clip in a kernel trace of `bench.py --clip ...`: kernels
     grouped by the frames each layer attends to (the sampler's call sequence and the layer
@@ -698,6 +730,9 @@ def main():
     args = parse()
     if args.summarize_profile:
         summarize_profile(args.summarize_profile, args.workload, args.qknorm)
+        return
+    if args.summarize_trace:
+        summarize_trace(args.summarize_trace, args.trace_name or "trace", args.trace_command or "")
         return
     if args.summarize_clip_profile:
         summarize_clip_profile(args.summarize_clip_profile, args)
