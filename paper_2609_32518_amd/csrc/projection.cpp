@@ -77,7 +77,7 @@ hipblasLtHandle_t lt_handle(int dev) {
 }
 
 constexpr size_t kLinearWorkspace = size_t(32) << 20;   // per device, for algorithms that want it
-constexpr int kCandidates = 16;
+constexpr int kCandidates = 64;
 
 // Device scratch of the GEMM library, one per (device, stream), allocated on the first call
 // that uses the pair: GEMMs enqueued on different streams may run at the same time, so they
