@@ -186,3 +186,24 @@ def random_shape_cases(n_cases: int = 48, seed: int = 2609) -> list:
                 f0 += C
         cases.append(dict(B=B, H=H, gh=gh, gw=gw, S=S, R=R, C=C, W=W, calls=calls))
     return cases
+
+
+def random_medium_cases(n_cases: int = 16, seed: int = 4242) -> list:
+    """Seeded medium configurations: grids 4x4 to 16x16, 1-6 heads, up to 3 sinks and 12-frame
+    windows, so walks run over tens of key tiles, through several runs of a wrapped ring and
+    on every schedule (one work-group per query tile, the balanced split, the equal split of
+    each query tile); call sequences as in random_shape_cases."""
+    rng = np.random.default_rng([seed, 9])
+    cases = []
+    for _ in range(n_cases):
+        B, H = int(rng.integers(1, 3)), int(rng.integers(1, 7))
+        gh, gw = int(rng.integers(4, 17)), int(rng.integers(4, 17))
+        S, C, W = int(rng.integers(0, 4)), int(rng.integers(1, 4)), int(rng.integers(0, 13))
+        R = W + C + int(rng.integers(0, 3))
+        calls, f0 = [], 0
+        for _ in range(int(rng.integers(4, 9))):
+            calls.append((f0, bool(rng.integers(0, 4) > 0), bool(rng.integers(0, 2))))
+            if rng.random() < 0.8:
+                f0 += C
+        cases.append(dict(B=B, H=H, gh=gh, gw=gw, S=S, R=R, C=C, W=W, calls=calls))
+    return cases

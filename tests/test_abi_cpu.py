@@ -331,13 +331,14 @@ def test_schedule_choice_follows_the_measured_costs():
 
 
 def test_random_shape_cases_are_valid_and_reach_both_schedules():
-    # the call sequences of the randomized GPU parity test, replayed on the host index and the
-    # oracle's cache model: every call is accepted by both with equal segments, and the cases
-    # reach the balanced schedule, the plain one, chunks across the sink boundary and single tokens
-    from tests.gpu_helpers import random_shape_cases
-    balanced = plain = straddle = 0
+    # the call sequences of the randomized GPU parity tests (small and medium shapes), replayed on
+    # the host index and the oracle's cache model: every call is accepted by both with equal
+    # segments, and the cases reach the plain schedule, the balanced one and its equal split of
+    # each query tile, chunks across the sink boundary and single tokens
+    from tests.gpu_helpers import random_medium_cases, random_shape_cases
+    balanced = plain = straddle = equal_split = 0
     cases = random_shape_cases()
-    for cs in cases:
+    for cs in cases + random_medium_cases():
         rc, h = _handle(cs["B"], cs["H"], cs["gh"], cs["gw"], cs["S"], cs["R"])
         assert rc == u.OK
         orc = KVCacheOracle(cs["B"], cs["H"], 128, cs["gh"], cs["gw"], cs["S"], cs["R"])
@@ -353,12 +354,15 @@ def test_random_shape_cases_are_valid_and_reach_both_schedules():
                 assert u.lib.unstep_attn_workspace_size(h, f0, C, W, ctypes.byref(b)) == u.OK
                 if use_split and b.value > 0:
                     balanced += 1
+                    groups = b.value // (2 * 256 * (128 + 2) * 4)
+                    qtiles = cs["B"] * cs["H"] * -(-C * cs["gh"] * cs["gw"] // 256)
+                    equal_split += groups % qtiles == 0 and groups // qtiles >= 2
                 else:
                     plain += 1
                 straddle += f0 < cs["S"] < f0 + C
         finally:
             u.lib.unstep_cache_destroy(h)
-    assert balanced >= 10 and plain >= 10 and straddle >= 2, (balanced, plain, straddle)
+    assert balanced >= 10 and plain >= 10 and straddle >= 2 and equal_split >= 5, (balanced, plain, straddle, equal_split)
     assert any(cs["gh"] * cs["gw"] == 1 for cs in cases)
 
 

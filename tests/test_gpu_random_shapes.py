@@ -9,7 +9,7 @@ import pytest
 import torch
 
 import synth
-from tests.gpu_helpers import LSE_ABS, Mirror, check_attention, host, log, random_shape_cases
+from tests.gpu_helpers import LSE_ABS, Mirror, check_attention, host, log, random_medium_cases, random_shape_cases
 
 pytestmark = pytest.mark.gpu
 
@@ -18,11 +18,20 @@ if not torch.cuda.is_available():
     pytest.skip("needs a GPU", allow_module_level=True)
 
 CASES = random_shape_cases()
+MEDIUM = random_medium_cases()
 
 
 @pytest.mark.parametrize("case", range(len(CASES)))
 def test_random_shape_stream(case):
-    cs = CASES[case]
+    _stream(CASES[case], case)
+
+
+@pytest.mark.parametrize("case", range(len(MEDIUM)))
+def test_random_medium_shape_stream(case):
+    _stream(MEDIUM[case], 100 + case)
+
+
+def _stream(cs, case):
     C, W = cs["C"], cs["W"]
     log(f"random shape {case}: " + " ".join(f"{k}={v}" for k, v in cs.items() if k != "calls"))
     m = Mirror(u, cs["B"], cs["H"], cs["gh"], cs["gw"], cs["S"], cs["R"])
