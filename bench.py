@@ -537,7 +537,7 @@ def oproj_bench(u, torch, args):
     xs = [torch.randn((M, K), generator=g, device=dev).to(torch.bfloat16) for _ in range(16)]   # 230 MB
     w32 = torch.randn((N, K), generator=g, device=dev) / math.sqrt(K)
     b = torch.randn((N,), generator=g, device=dev).to(torch.bfloat16)
-    r = u.vo_rank(K)
+    r = 1413                     # the paper's V/O rank: round(0.92 * 1536) (App. A.4)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     _, w, _ = u.unstep_svd_truncate(w32, r)

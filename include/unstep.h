@@ -48,7 +48,8 @@ typedef enum {
   UNSTEP_E_RANGE = -3,  /* frame index / window / chunk outside what the cache can hold  */
   UNSTEP_E_STATE = -4,  /* cache state forbids the call (gap, evicted or missing frame)  */
   UNSTEP_E_HIP = -5,    /* the HIP runtime reported an error (message from HIP)          */
-  UNSTEP_E_ALIGN = -6   /* a pointer is not 16-byte aligned or a stride not a multiple of 8 */
+  UNSTEP_E_ALIGN = -6,  /* a pointer is not 16-byte aligned or a stride not a multiple of 8 */
+  UNSTEP_E_HOST = -7    /* a host-side failure, e.g. out of host memory (no state changed)  */
 } unstep_status;
 
 #define UNSTEP_HEAD_DIM 128

@@ -24,9 +24,9 @@ import torch
 HEAD_DIM = 128
 MAX_SEGMENTS = 4
 
-OK, E_NULL, E_SHAPE, E_RANGE, E_STATE, E_HIP, E_ALIGN = 0, -1, -2, -3, -4, -5, -6
+OK, E_NULL, E_SHAPE, E_RANGE, E_STATE, E_HIP, E_ALIGN, E_HOST = 0, -1, -2, -3, -4, -5, -6, -7
 STATUS_NAMES = {OK: "OK", E_NULL: "E_NULL", E_SHAPE: "E_SHAPE", E_RANGE: "E_RANGE", E_STATE: "E_STATE",
-                E_HIP: "E_HIP", E_ALIGN: "E_ALIGN"}
+                E_HIP: "E_HIP", E_ALIGN: "E_ALIGN", E_HOST: "E_HOST"}
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libunstep.so")
 
@@ -103,6 +103,23 @@ def _used_on(stream: Optional[torch.cuda.Stream], *tensors: Optional[torch.Tenso
             t.record_stream(stream)
 
 
+def _need(t: Optional[torch.Tensor], name: str, shape: Tuple[int, ...], dtype: torch.dtype, device: torch.device,
+          contiguous: bool = True) -> None:
+    """Reject a tensor the kernels would misread: wrong dtype, shape, device or layout.  The
+    library sees only a pointer, so these checks are the binding's half of the contract of
+    include/unstep.h (the library checks sizes, alignment and the cache state)."""
+    if t is None:
+        raise ValueError(f"{name} is required")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if t.device != device:
+        raise ValueError(f"{name} is on {t.device}, the cache on {device}")
+    if contiguous and not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+
+
 def version() -> int:
     return lib.unstep_version()
 
@@ -174,6 +191,9 @@ class Cache:
         shape = (batch, n_heads, self.slots, head_dim)
         self.k = k_cache if k_cache is not None else torch.zeros(shape, dtype=torch.bfloat16, device=device)
         self.v = v_cache if v_cache is not None else torch.zeros(shape, dtype=torch.bfloat16, device=device)
+        self.device = self.k.device
+        _need(self.k, "k_cache", shape, torch.bfloat16, self.device)
+        _need(self.v, "v_cache", shape, torch.bfloat16, self.device)
         h = _vp()
         _check(lib.unstep_cache_create(ctypes.byref(h), batch, n_heads, head_dim, grid_h, grid_w, sink_frames,
                                        ring_frames, self.k.data_ptr(), self.v.data_ptr()))
@@ -220,21 +240,53 @@ class Cache:
         return self._ws
 
     # -- step path --------------------------------------------------------------------
-    @staticmethod
-    def _strides(x: torch.Tensor) -> Tuple[int, int]:
-        if x.dtype != torch.bfloat16 or x.dim() != 4 or x.shape[-1] != HEAD_DIM or x.stride(-1) != 1:
-            raise ValueError("q/k/v must be bf16 [B, N, H, 128] with unit stride on the last axis")
+    def _strides(self, x: torch.Tensor, name: str, n_frames: int) -> Tuple[int, int]:
+        """(token, head) element strides of a q/k/v input [B, n_frames*T, H, 128]: any token and
+        head strides with unit stride on the last axis and the batch stride N * token stride
+        (e.g. views into a fused [B, N, 3, H, 128] projection output)."""
+        N = n_frames * self.T
+        _need(x, name, (self.B, N, self.H, HEAD_DIM), torch.bfloat16, self.device, contiguous=False)
+        if x.stride(3) != 1 or (self.B > 1 and x.stride(0) != N * x.stride(1)):
+            raise ValueError(f"{name} must have unit stride on the last axis and batch stride N * token stride")
         return x.stride(1), x.stride(2)
+
+    def _qkv_strides(self, q: Optional[torch.Tensor], k: torch.Tensor, v: torch.Tensor,
+                     n_frames: int) -> Tuple[int, int]:
+        ts, hs = self._strides(k, "k", n_frames)
+        if self._strides(v, "v", n_frames) != (ts, hs) or (q is not None and self._strides(q, "q", n_frames) != (ts, hs)):
+            raise ValueError("q, k, v must share strides")
+        return ts, hs
+
+    def _tables(self, cos_t: torch.Tensor, sin_t: torch.Tensor, n_frames: int) -> None:
+        for t, name in ((cos_t, "cos_t"), (sin_t, "sin_t")):
+            _need(t, name, (n_frames * self.T, HEAD_DIM // 2), torch.float32, self.device)
+
+    def _chunk_out(self, t: Optional[torch.Tensor], name: str, n_frames: int) -> torch.Tensor:
+        """A caller-given bf16 [B, N, H, 128] output checked, or a new one."""
+        shape = (self.B, n_frames * self.T, self.H, HEAD_DIM)
+        if t is None:
+            return torch.empty(shape, dtype=torch.bfloat16, device=self.device)
+        _need(t, name, shape, torch.bfloat16, self.device)
+        return t
+
+    def _lse(self, lse: Optional[torch.Tensor], n_frames: int) -> None:
+        if lse is not None:
+            _need(lse, "lse", (self.B, self.H, n_frames * self.T), torch.float32, self.device)
+
+    def _workspace_bytes(self, workspace: Optional[torch.Tensor]) -> int:
+        if workspace is None:
+            return 0
+        if workspace.device != self.device or not workspace.is_contiguous():
+            raise ValueError("workspace must be a contiguous tensor on the cache's device")
+        return workspace.numel() * workspace.element_size()
 
     def unstep_kv_append(self, start_frame: int, n_frames: int, q: Optional[torch.Tensor], k: torch.Tensor,
                          v: torch.Tensor, cos_t: torch.Tensor, sin_t: torch.Tensor,
                          q_rot: Optional[torch.Tensor] = None, stream=None) -> Optional[torch.Tensor]:
-        ts, hs = self._strides(k)
-        if self._strides(v) != (ts, hs) or (q is not None and self._strides(q) != (ts, hs)):
-            raise ValueError("q, k, v must share strides")
-        if q is not None and q_rot is None:
-            q_rot = torch.empty((self.B, n_frames * self.T, self.H, HEAD_DIM), dtype=torch.bfloat16,
-                                device=k.device)
+        ts, hs = self._qkv_strides(q, k, v, n_frames)
+        self._tables(cos_t, sin_t, n_frames)
+        if q is not None:
+            q_rot = self._chunk_out(q_rot, "q_rot", n_frames)
         _check(lib.unstep_kv_append(self.handle, start_frame, n_frames, _ptr(q), k.data_ptr(), v.data_ptr(), ts, hs,
                                     cos_t.data_ptr(), sin_t.data_ptr(), _ptr(q_rot), _stream(stream)))
         _used_on(stream, q_rot)
@@ -247,15 +299,12 @@ class Cache:
                                 stream=None) -> Optional[torch.Tensor]:
         """unstep_kv_append with the RMS normalisation of q and k over each token's H*128 channels
         (weights: bf16 [H*128])."""
-        ts, hs = self._strides(k)
-        if self._strides(v) != (ts, hs) or (q is not None and self._strides(q) != (ts, hs)):
-            raise ValueError("q, k, v must share strides")
-        for w in (k_norm_weight, q_norm_weight):
-            if w is not None and (w.dtype != torch.bfloat16 or w.numel() != self.H * HEAD_DIM or not w.is_contiguous()):
-                raise ValueError("norm weights must be contiguous bf16 [H*128]")
-        if q is not None and q_rot is None:
-            q_rot = torch.empty((self.B, n_frames * self.T, self.H, HEAD_DIM), dtype=torch.bfloat16,
-                                device=k.device)
+        ts, hs = self._qkv_strides(q, k, v, n_frames)
+        self._tables(cos_t, sin_t, n_frames)
+        _need(k_norm_weight, "k_norm_weight", (self.H * HEAD_DIM,), torch.bfloat16, self.device)
+        if q is not None:
+            _need(q_norm_weight, "q_norm_weight", (self.H * HEAD_DIM,), torch.bfloat16, self.device)
+            q_rot = self._chunk_out(q_rot, "q_rot", n_frames)
         _check(lib.unstep_kv_append_qknorm(self.handle, start_frame, n_frames, _ptr(q), k.data_ptr(), v.data_ptr(),
                                            ts, hs, cos_t.data_ptr(), sin_t.data_ptr(), _ptr(q_norm_weight),
                                            k_norm_weight.data_ptr(), norm_eps, _ptr(q_rot), _stream(stream)))
@@ -266,11 +315,12 @@ class Cache:
                            out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
                            softmax_scale: float = 0.0, workspace: Optional[torch.Tensor] = None,
                            use_split: bool = True, stream=None) -> torch.Tensor:
-        if out is None:
-            out = torch.empty_like(q_rot)
+        _need(q_rot, "q_rot", (self.B, n_frames * self.T, self.H, HEAD_DIM), torch.bfloat16, self.device)
+        out = self._chunk_out(out, "out", n_frames)
+        self._lse(lse, n_frames)
         if workspace is None and use_split:
             workspace = self.workspace(start_frame, n_frames, window_frames)
-        ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+        ws_bytes = self._workspace_bytes(workspace)
         _check(lib.unstep_window_attn(self.handle, start_frame, n_frames, window_frames, q_rot.data_ptr(),
                                       out.data_ptr(), _ptr(lse), softmax_scale, _ptr(workspace), ws_bytes,
                                       _stream(stream)))
@@ -282,17 +332,16 @@ class Cache:
                     out: Optional[torch.Tensor] = None, lse: Optional[torch.Tensor] = None,
                     softmax_scale: float = 0.0, workspace: Optional[torch.Tensor] = None, use_split: bool = True,
                     stream=None) -> torch.Tensor:
-        ts, hs = self._strides(q)
-        if self._strides(k) != (ts, hs) or self._strides(v) != (ts, hs):
-            raise ValueError("q, k, v must share strides")
-        N = n_frames * self.T
-        if q_rot is None:
-            q_rot = torch.empty((self.B, N, self.H, HEAD_DIM), dtype=torch.bfloat16, device=q.device)
-        if out is None:
-            out = torch.empty((self.B, N, self.H, HEAD_DIM), dtype=torch.bfloat16, device=q.device)
+        if q is None:
+            raise ValueError("unstep_step needs q")
+        ts, hs = self._qkv_strides(q, k, v, n_frames)
+        self._tables(cos_t, sin_t, n_frames)
+        q_rot = self._chunk_out(q_rot, "q_rot", n_frames)
+        out = self._chunk_out(out, "out", n_frames)
+        self._lse(lse, n_frames)
         if workspace is None and use_split:
             workspace = self._step_workspace(start_frame, n_frames, window_frames)
-        ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+        ws_bytes = self._workspace_bytes(workspace)
         _check(lib.unstep_step(self.handle, start_frame, n_frames, window_frames, q.data_ptr(), k.data_ptr(),
                                v.data_ptr(), ts, hs, cos_t.data_ptr(), sin_t.data_ptr(), q_rot.data_ptr(),
                                out.data_ptr(), _ptr(lse), softmax_scale, _ptr(workspace), ws_bytes,
@@ -316,12 +365,6 @@ def unstep_shift_schedule(n_steps: int = 4, shift: float = 5.0):
 
 
 # -- V/O truncated SVD and the projection after attention (Section 3.5, Appendix A.4) -------------
-def vo_rank(m: int, retain: float = 0.92) -> int:
-    """r = round(retain * m): 1413 for the model's 1536-wide projections."""
-    import math
-    return int(math.floor(retain * m + 0.5))
-
-
 def unstep_svd_truncate(w: torch.Tensor, rank: int, bf16: bool = True, stream=None):
     """Init-time rank-r reconstruction of a float32 [rows, cols] device weight.  Returns
     (w_r float32, w_r bf16 or None, singular values as a float32 numpy array)."""
@@ -347,8 +390,13 @@ def unstep_linear(x: torch.Tensor, w: torch.Tensor, bias: Optional[torch.Tensor]
     if x.shape[-1] != K or (bias is not None and bias.shape != (N,)):
         raise ValueError("shapes: x [..., K], w [N, K], bias [N]")
     M = x.numel() // K
+    for t in (w,) + ((bias,) if bias is not None else ()):
+        if t.device != x.device:
+            raise ValueError("x, w, bias must be on one device")
     if out is None:
         out = torch.empty(x.shape[:-1] + (N,), dtype=torch.bfloat16, device=x.device)
+    else:
+        _need(out, "out", tuple(x.shape[:-1]) + (N,), torch.bfloat16, x.device)
     _check(lib.unstep_linear(x.data_ptr(), w.data_ptr(), _ptr(bias), out.data_ptr(), M, N, K, _stream(stream)))
     _used_on(stream, out)
     return out
@@ -393,8 +441,10 @@ def unstep_renoise(x: torch.Tensor, eps: torch.Tensor, sigma: float, out: Option
         _latent(t)
     if eps.shape != x.shape:
         raise ValueError("x and eps must have the same shape")
+    if eps.device != x.device:
+        raise ValueError("x and eps must be on one device")
     out = torch.empty_like(x) if out is None else out
-    _latent(out)
+    _need(out, "out", tuple(x.shape), torch.bfloat16, x.device)
     _check(lib.unstep_renoise(x.data_ptr(), eps.data_ptr(), sigma, out.data_ptr(), x.numel(), _stream(stream)))
     _used_on(stream, out)
     return out
@@ -407,8 +457,10 @@ def unstep_emit(x_tilde: torch.Tensor, v: torch.Tensor, sigma: float, out: Optio
         _latent(t)
     if v.shape != x_tilde.shape:
         raise ValueError("x_tilde and v must have the same shape")
+    if v.device != x_tilde.device:
+        raise ValueError("x_tilde and v must be on one device")
     out = torch.empty_like(x_tilde) if out is None else out
-    _latent(out)
+    _need(out, "out", tuple(x_tilde.shape), torch.bfloat16, x_tilde.device)
     _check(lib.unstep_emit(x_tilde.data_ptr(), v.data_ptr(), sigma, out.data_ptr(), x_tilde.numel(), _stream(stream)))
     _used_on(stream, out)
     return out

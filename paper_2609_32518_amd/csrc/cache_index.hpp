@@ -41,13 +41,20 @@ class CacheIndex {
   int32_t slot(int32_t f) const { return f < S_ ? f : S_ + (f - S_) % R_; }
   bool resident(int32_t f) const { return f >= 0 && frame_of_slot_[slot(f)] == f; }
 
-  // Validation of an append of frames [f0, f0 + C); UNSTEP_OK or a status + message.
+  // Frames of [lo, hi) that live in the ring (frame >= S), counted without visiting them.
+  int64_t ring_count(int64_t lo, int64_t hi) const {
+    const int64_t first = lo > S_ ? lo : S_;
+    return hi > first ? hi - first : 0;
+  }
+
+  // Validation of an append of frames [f0, f0 + C); UNSTEP_OK or a status + message.  The
+  // sizes are checked arithmetically before any loop over frames, so a huge request costs
+  // nothing and allocates nothing.
   int check_append(int32_t f0, int32_t C, std::string* why) const {
     if (C < 1) return fail(UNSTEP_E_SHAPE, "empty chunk (n_frames < 1)", why);
     if (f0 < 0) return fail(UNSTEP_E_RANGE, "negative start frame", why);
-    int64_t ring_frames = 0;
-    for (int64_t f = f0; f < int64_t(f0) + C; ++f) ring_frames += (f >= S_);
-    if (ring_frames > R_) return fail(UNSTEP_E_RANGE, "chunk has more ring frames than the ring holds", why);
+    if (ring_count(f0, int64_t(f0) + C) > R_)
+      return fail(UNSTEP_E_RANGE, "chunk has more ring frames than the ring holds", why);
     if (int64_t(f0) + C - 1 > INT32_MAX - 1) return fail(UNSTEP_E_RANGE, "frame index overflow", why);
     if (f0 > newest_ + 1) return fail(UNSTEP_E_STATE, "gap: chunk starts after newest stored frame + 1", why);
     for (int32_t f = f0; f < f0 + C; ++f)
@@ -69,23 +76,26 @@ class CacheIndex {
     if (int64_t(f0) + C - 1 > INT32_MAX - 1) return fail(UNSTEP_E_RANGE, "frame index overflow", why);
     const int32_t lo = f0 - W > 0 ? f0 - W : 0;
     const int32_t n_sink = S_ < lo ? S_ : lo;
+    // the sinks lie below S; the window and the chunk may not need more ring slots than exist
+    if (ring_count(lo, int64_t(f0) + C) > R_)
+      return fail(UNSTEP_E_RANGE, "window plus chunk has more ring frames than the ring holds", why);
     frames->clear();
     for (int32_t f = 0; f < n_sink; ++f) frames->push_back(f);
     for (int32_t f = lo; f < f0 + C; ++f) frames->push_back(f);
-    int64_t ring_frames = 0;
-    for (int32_t f : *frames) ring_frames += (f >= S_);
-    if (ring_frames > R_) return fail(UNSTEP_E_RANGE, "window plus chunk has more ring frames than the ring holds", why);
     for (int32_t f : *frames)
       if (!resident(f)) return fail(UNSTEP_E_STATE, "frame " + std::to_string(f) + " is not in the cache", why);
     return UNSTEP_OK;
   }
 
-  // Number of retained frames from the window formula alone (no residency check).
+  // Number of retained frames from the window formula alone (no residency check; the ring
+  // must hold the window and the chunk, so the count is at most S + R).
   int retained_count(int32_t f0, int32_t C, int32_t W, int32_t* count, std::string* why) const {
     if (C < 1) return fail(UNSTEP_E_SHAPE, "empty chunk (n_frames < 1)", why);
     if (f0 < 0 || W < 0) return fail(UNSTEP_E_RANGE, "negative start frame or window", why);
     if (int64_t(f0) + C - 1 > INT32_MAX - 1) return fail(UNSTEP_E_RANGE, "frame index overflow", why);
     const int32_t lo = f0 - W > 0 ? f0 - W : 0;
+    if (ring_count(lo, int64_t(f0) + C) > R_)
+      return fail(UNSTEP_E_RANGE, "window plus chunk has more ring frames than the ring holds", why);
     *count = (S_ < lo ? S_ : lo) + (f0 + C - lo);
     return UNSTEP_OK;
   }

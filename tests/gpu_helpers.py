@@ -81,10 +81,11 @@ class Mirror:
         self.orc = KVCacheOracle(B, H, 128, grid_h, grid_w, S, R)
         self.tables = u.RopeTableCache(device)
 
-    def inputs(self, C: int, key, q_scale=1.0, v_bits: Optional[np.ndarray] = None, q_zero=False):
+    def inputs(self, C: int, key, q_scale=1.0, v_bits: Optional[np.ndarray] = None, q_zero=False,
+               k_bits: Optional[np.ndarray] = None):
         shape = (self.B, C * self.T, self.H, 128)
         q = np.zeros(shape, np.uint16) if q_zero else synth.normal_bf16(shape, tuple(key) + (synth.Q,), q_scale)
-        k = synth.normal_bf16(shape, tuple(key) + (synth.K,))
+        k = synth.normal_bf16(shape, tuple(key) + (synth.K,)) if k_bits is None else k_bits
         v = synth.normal_bf16(shape, tuple(key) + (synth.V,)) if v_bits is None else v_bits
         return q, k, v
 

@@ -298,7 +298,6 @@ def test_svd_and_linear_argument_errors():
     assert g(p[0], p[1], None, p[2], 4, 8, 12, None) == u.E_SHAPE
     assert g(p[0], p[1], None, p[2], 4, 12, 8, None) == u.E_SHAPE
     assert g(p[0], p[1], p[3] + 2, p[2], 4, 8, 8, None) == u.E_ALIGN
-    assert u.vo_rank(1536) == 1413
 
 
 def test_schedule_choice_follows_the_measured_costs():
@@ -379,5 +378,95 @@ def test_attention_rejects_more_query_tiles_than_one_launch_holds():
         assert b"query tiles" in u.lib.unstep_last_error()
         b = ctypes.c_size_t()
         assert u.lib.unstep_attn_workspace_size(h, 1, 1, 1, ctypes.byref(b)) == u.OK
+    finally:
+        u.lib.unstep_cache_destroy(h)
+
+
+def test_binding_rejects_tensors_the_kernels_would_misread():
+    # the library sees only pointers: the binding checks dtype, shape, device and layout of every
+    # tensor against the handle before calling it (a CPU-side cache here: no call gets that far)
+    B, H, gh, gw, S, R = 1, 2, 4, 6, 0, 9
+    c = u.Cache(B, H, gh, gw, S, R, device="cpu")
+    T, C = gh * gw, 3
+    N = C * T
+    bf = dict(dtype=torch.bfloat16)
+    q = torch.zeros((B, N, H, 128), **bf)
+    k, v = q.clone(), q.clone()
+    cos_t = torch.zeros((N, 64), dtype=torch.float32)
+    sin_t = cos_t.clone()
+    bad = {
+        "k dtype": dict(k=k.float()),
+        "k tokens": dict(k=torch.zeros((B, N - 1, H, 128), **bf)),
+        "k heads": dict(k=torch.zeros((B, N, H + 1, 128), **bf)),
+        "k batch": dict(k=torch.zeros((B + 1, N, H, 128), **bf)),
+        "k device": dict(k=torch.zeros((B, N, H, 128), device="meta", **bf)),
+        "k last stride": dict(k=torch.zeros((B, N, 128, H), **bf).transpose(2, 3)),
+        "v strides": dict(v=torch.zeros((B, N, 2, H, 128), **bf)[:, :, 0]),
+        "cos rows": dict(cos_t=torch.zeros((N - 1, 64))),
+        "sin dtype": dict(sin_t=torch.zeros((N, 64), dtype=torch.float64)),
+        "q_rot shape": dict(q_rot=torch.zeros((B, N, H, 64), **bf)),
+        "q_rot layout": dict(q_rot=torch.zeros((B, H, N, 128), **bf).transpose(1, 2)),
+    }
+    for what, kw in bad.items():
+        args = dict(q=q, k=k, v=v, cos_t=cos_t, sin_t=sin_t, q_rot=None)
+        args.update(kw)
+        with pytest.raises(ValueError):
+            c.unstep_kv_append(6, C, args["q"], args["k"], args["v"], args["cos_t"], args["sin_t"],
+                               q_rot=args["q_rot"])
+        with pytest.raises(ValueError):
+            c.unstep_step(6, C, 6, args["q"], args["k"], args["v"], args["cos_t"], args["sin_t"],
+                          q_rot=args["q_rot"])
+    wn = torch.ones(H * 128, **bf)
+    for kw in (dict(k_norm_weight=torch.ones(H * 128 - 8, **bf)), dict(q_norm_weight=torch.ones(H * 128)),
+               dict(q_norm_weight=None)):
+        args = dict(q_norm_weight=wn, k_norm_weight=wn)
+        args.update(kw)
+        with pytest.raises(ValueError):
+            c.unstep_kv_append_qknorm(6, C, q, k, v, cos_t, sin_t, args["q_norm_weight"], args["k_norm_weight"])
+    # attention: q_rot, out, lse
+    for kw in (dict(q_rot=torch.zeros((B, N + 1, H, 128), **bf)),
+               dict(q_rot=torch.zeros((B, H, N, 128), **bf).transpose(1, 2)),
+               dict(out=torch.zeros((B, N, H, 128), dtype=torch.float16)),
+               dict(out=torch.zeros((B, N, 128, H), **bf).transpose(2, 3)),
+               dict(lse=torch.zeros((B, N, H))),
+               dict(lse=torch.zeros((B, H, N), dtype=torch.float16))):
+        args = dict(q_rot=q, out=None, lse=None)
+        args.update(kw)
+        with pytest.raises(ValueError):
+            c.unstep_window_attn(6, C, 6, args["q_rot"], out=args["out"], lse=args["lse"])
+        with pytest.raises(ValueError):
+            c.unstep_step(6, C, 6, q, k, v, cos_t, sin_t, q_rot=args["q_rot"], out=args["out"], lse=args["lse"])
+    # caller-given cache buffers of the wrong size or type
+    with pytest.raises(ValueError):
+        u.Cache(B, H, gh, gw, S, R, device="cpu", k_cache=torch.zeros((B, H, (S + R) * T - 1, 128), **bf))
+    with pytest.raises(ValueError):
+        u.Cache(B, H, gh, gw, S, R, device="cpu", v_cache=torch.zeros((B, H, (S + R) * T, 128)))
+    # nothing was recorded by the rejected calls
+    assert c.frame_map() == ([-1] * (S + R), -1)
+    # clean-cache updates and the projection: shapes of caller outputs and devices
+    x = torch.zeros((2, 8), **bf)
+    with pytest.raises(ValueError):
+        u.unstep_renoise(x, x, 0.1, out=torch.zeros((2, 16), **bf))
+    with pytest.raises(ValueError):
+        u.unstep_emit(x, torch.zeros((2, 8), device="meta", **bf), 0.1)
+    with pytest.raises(ValueError):
+        u.unstep_linear(torch.zeros((4, 8), **bf), torch.zeros((8, 8), **bf), out=torch.zeros((4, 16), **bf))
+
+
+def test_huge_frame_requests_fail_fast_without_allocating():
+    # a window or chunk of ~2^31 frames is rejected from the frame counts alone (no frame list
+    # is built), so the call returns E_RANGE at once instead of exhausting host memory
+    rc, h = _handle(1, 1, 2, 3, 2, 4)
+    assert rc == u.OK
+    try:
+        assert u.lib.unstep_cache_advance(h, 0, 3) == u.OK
+        big = 2_000_000_000
+        assert _segments(h, big, 1, big)[0] == u.E_RANGE
+        assert _segments(h, 0, big, 0)[0] == u.E_RANGE
+        assert u.lib.unstep_cache_advance(h, 0, big) == u.E_RANGE
+        ws = u._sz()
+        assert u.lib.unstep_attn_workspace_size(h, big, 1, big, ctypes.byref(ws)) == u.E_RANGE
+        assert u.lib.unstep_attn_workspace_size(h, 0, big, 0, ctypes.byref(ws)) == u.E_RANGE
+        assert _frame_map(h, 6) == ([0, 1, 2, -1, -1, -1], 2)
     finally:
         u.lib.unstep_cache_destroy(h)

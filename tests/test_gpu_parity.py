@@ -65,10 +65,10 @@ def test_full_chunk(u, use_split):
     assert np.array_equal(host(q_rot), q_rot_ref)
     m.check_cache("full_chunk")
     assert m.lib.segments(wl.f0, wl.C, wl.W) == [(0, 18720)]
-    idx = sample_queries(wl.n_query, 192, 7)
-    want, want_lse = m.expected(q_rot_ref, wl.f0, wl.C, wl.W, query_idx=idx)
-    log(f"  {check_attention(host(out)[:, idx], want, 'full_chunk')}")
-    assert np.max(np.abs(lse.cpu().numpy()[:, :, idx] - want_lse)) <= LSE_ABS
+    # every query x head x dim against the oracle
+    want, want_lse = m.expected(q_rot_ref, wl.f0, wl.C, wl.W)
+    log(f"  {check_attention(host(out), want, 'full_chunk')}")
+    assert np.max(np.abs(lse.cpu().numpy() - want_lse)) <= LSE_ABS
 
 
 def test_unwindowed(u):
@@ -82,17 +82,15 @@ def test_unwindowed(u):
     torch.cuda.synchronize()
     assert np.array_equal(host(q_rot), q_rot_ref)
     m.check_cache("unwindowed")
-    idx = sample_queries(wl.n_query, 128, 8)
-    want, want_lse = m.expected(q_rot_ref, wl.f0, wl.C, wl.W, query_idx=idx)
-    log(f"  {check_attention(host(out)[:, idx], want, 'unwindowed')}")
-    assert np.max(np.abs(lse.cpu().numpy()[:, :, idx] - want_lse)) <= LSE_ABS
+    want, want_lse = m.expected(q_rot_ref, wl.f0, wl.C, wl.W)
+    log(f"  {check_attention(host(out), want, 'unwindowed')}")
+    assert np.max(np.abs(lse.cpu().numpy() - want_lse)) <= LSE_ABS
 
 
 @pytest.mark.parametrize("group", [0, 1, 2])
 def test_short_window_refine_30_layers(u, group):
     wl = synth.WORKLOADS["short_refine"]
     log(f"short_refine: layers {10 * group}..{10 * group + 9} of 30, 2 passes, chunk@12 W=3 R=6 (wraps)")
-    idx = sample_queries(wl.n_query, 48, 9)
     for layer in range(10 * group, 10 * group + 10):
         m = Mirror(u, wl.B, wl.H, wl.grid_h, wl.grid_w, wl.S, wl.R)
         # frames 0..8 are evicted before the chunk at 12 reads the cache; 9..11 are the window
@@ -103,8 +101,10 @@ def test_short_window_refine_30_layers(u, group):
             assert np.array_equal(host(q_rot), q_rot_ref)
             if layer % 10 == 0 or p == wl.passes - 1:
                 m.check_cache(f"short_refine layer {layer} pass {p}")
-            want, _ = m.expected(q_rot_ref, wl.f0, wl.C, wl.W, query_idx=idx, heads=[layer % 12])
-            got = host(out)[:, idx][:, :, [layer % 12]]
+            # every query of one head per call (all heads in the first layer of each group)
+            heads = list(range(wl.H)) if layer % 10 == 0 else [layer % 12]
+            want, _ = m.expected(q_rot_ref, wl.f0, wl.C, wl.W, heads=heads)
+            got = host(out)[:, :, heads]
             st = check_attention(got, want, f"short_refine layer {layer} pass {p}")
         assert m.lib.segments(wl.f0, wl.C, wl.W) == [(3 * 1560, 3 * 1560), (0, 3 * 1560)]
         if layer % 10 == 0:
@@ -121,7 +121,9 @@ def test_rolling_stream_60_chunks(u):
         torch.cuda.synchronize()
         assert np.array_equal(host(q_rot), q_rot_ref), c
         m.check_cache(f"rolling chunk {c}")
-        idx = sample_queries(wl.n_query, 24, 100 + c)
+        # every query at the empty start, the first full window, the first wrap and the end;
+        # a sample of rows elsewhere
+        idx = np.arange(wl.n_query) if c in (0, 11, 12, 59) else sample_queries(wl.n_query, 24, 100 + c)
         want, want_lse = m.expected(q_rot_ref, c, 1, wl.W, query_idx=idx)
         st = check_attention(host(out)[:, idx], want, f"rolling chunk {c}")
         if with_lse:
@@ -137,12 +139,54 @@ def test_paper_default_sinks(u):
     _prefill(m, wl, 6, wl.f0)
     q_rot, out, lse, q_rot_ref = m.step(wl.f0, wl.C, wl.W, (6, 100), lse=True)
     torch.cuda.synchronize()
+    assert np.array_equal(host(q_rot), q_rot_ref)
     m.check_cache("paper_default")
     assert sum(l for _, l in m.lib.segments(wl.f0, wl.C, wl.W)) == 14040
-    idx = sample_queries(wl.n_query, 128, 10)
-    want, want_lse = m.expected(q_rot_ref, wl.f0, wl.C, wl.W, query_idx=idx)
-    assert np.max(np.abs(lse.cpu().numpy()[:, :, idx] - want_lse)) <= LSE_ABS
-    log(f"  {check_attention(host(out)[:, idx], want, 'paper_default')}")
+    want, want_lse = m.expected(q_rot_ref, wl.f0, wl.C, wl.W)
+    assert np.max(np.abs(lse.cpu().numpy() - want_lse)) <= LSE_ABS
+    log(f"  {check_attention(host(out), want, 'paper_default')}")
+
+
+# Exact-max re-walk.  The kernel fixes each row's exponent offset at the maximum of the first
+# key tile of its range; a row whose scores later exceed that offset by more than
+# 64 / (scale log2 e) ~ 502 raw units overflows the 2^64 row-sum guard, and the work-group
+# walks its range again, first for the exact row maximum, then for the sums.  Here one head
+# gets needle keys: raw keys drawn N(0, 40^2) at several tokens of the chunk (the end of the
+# key range), so that about one query in eight scores more than 530 on them.  Run at the
+# full-frame shape on the plain schedule (one work-group per query tile, a single run of
+# cache rows) and at the unwindowed shape on both schedules; every element against the oracle.
+@pytest.mark.parametrize("workload,use_split", [("full_chunk", False), ("unwindowed", True),
+                                                ("unwindowed", False)])
+def test_exact_max_rewalk(u, workload, use_split):
+    wl = synth.WORKLOADS[workload]
+    log(f"rewalk: {workload} split={use_split}, needle keys in head 0")
+    m = Mirror(u, wl.B, wl.H, wl.grid_h, wl.grid_w, wl.S, wl.R)
+    _prefill(m, wl, 17, wl.f0)
+    if use_split:
+        assert m.lib.workspace_bytes(wl.f0, wl.C, wl.W) > 0
+    key = (17, 100)
+    shape = (wl.B, wl.n_query, wl.H, 128)
+    k = synth.normal_bf16(shape, key + (synth.K,))
+    needles = [100, 1100, 2100, 3100, 4100]
+    for j, t in enumerate(needles):
+        k[0, t, 0] = synth.normal_bf16((128,), key + (50 + j,), scale=40.0)
+    q_rot, out, lse, q_rot_ref = m.step(wl.f0, wl.C, wl.W, key, use_split=use_split, lse=True, k_bits=k)
+    torch.cuda.synchronize()
+    assert np.array_equal(host(q_rot), q_rot_ref)
+    m.check_cache(f"rewalk {workload}")
+    # the construction does trigger the guard: some row of head 0 scores more than 502 raw units
+    # above the maximum of its first key tile (the range starts at logical key 0 on the plain
+    # schedule)
+    rows = m.orc.key_rows(wl.f0, wl.C, wl.W)
+    qh = numerics.bf16_to_f64(q_rot_ref[0, :, 0])
+    s_first = qh @ numerics.bf16_to_f64(m.orc.k[0, 0, rows[:64]]).T
+    s_needle = qh @ numerics.bf16_to_f64(m.orc.k[0, 0, rows[-wl.n_query:][needles]]).T
+    jump = s_needle.max(axis=1) - s_first.max(axis=1)
+    log(f"  rows past the guard: {int((jump > 64 / (128 ** -0.5 * math.log2(math.e))).sum())} of {wl.n_query}")
+    assert (jump > 530).sum() > wl.n_query // 20
+    want, want_lse = m.expected(q_rot_ref, wl.f0, wl.C, wl.W)
+    log(f"  {check_attention(host(out), want, 'rewalk ' + workload)}")
+    assert np.max(np.abs(lse.cpu().numpy() - want_lse)) <= LSE_ABS
 
 
 @pytest.mark.parametrize("use_split", [True, False])

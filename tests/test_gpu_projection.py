@@ -71,7 +71,7 @@ def test_svd_truncation_well_conditioned(m, n, r):
 
 def test_svd_truncation_gaussian_weight_at_the_paper_rank():
     # no gap at the cut: the truncation is less well conditioned, the bound scales with it
-    r = u.vo_rank(1536)
+    r = svd.rank_for(1536)                        # the paper's rank, 1413
     w = _gaussian(1536, 1536, 7)
     wr_d, wb_d, sig = u.unstep_svd_truncate(torch.from_numpy(w).cuda(), r)
     torch.cuda.synchronize()
