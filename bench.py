@@ -1,15 +1,20 @@
 """Benchmark of the windowed-attention chunk step on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload full_chunk]
-                    [--sets 4] [--no-cpu-baseline]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload NAME]
+                    [--sub-steps K2] [--sets 6] [--no-cpu-baseline]
 
 A step is one whole pass of the hot path over one chunk: the fused RoPE + KV append
 and the windowed attention (unstep_step).  The default workload is the full-frame
 chunk: 12 heads of width 128, a 30x52 token grid, a 3-frame chunk (4680 queries) at
 latent frame 9 over 9 prior frames (18720 retained keys).  Other workloads:
 unwindowed (32760 keys), paper_default (3 sinks + 6 recent frames, 14040 keys),
-short_refine (one step = 30 layers x 2 calls over 9360 keys) and rolling (one step =
-60 one-frame chunks through a 12-frame ring from empty).
+short_refine (one step = 30 layers x 2 calls over 9360 keys), rolling (one step =
+60 one-frame chunks through a 12-frame ring from empty) and tiny (2 heads, 4x6 grid).
+Without --workload the run times the full-frame chunk as the headline (`value`,
+`roofline`, `cpu_baseline`) and then every other workload, each as a record under
+`workloads` (attention and append per call with their roofline fractions, the step; the
+short-window refine also its 60-call attention total, the rolling stream the mean, min and
+max of its per-chunk attention times); --workload NAME times only that one.
 
 Inputs are synthetic, seeded N(0,1) bf16, resident in HBM before timing.  Several
 buffer sets (cache + inputs + outputs) are rotated so that consecutive steps do not
@@ -44,7 +49,11 @@ def parse():
     p.add_argument("--steps", type=int, default=50)
     # the GPU settles its clock under sustained MFMA load within ~20 ms: warm up past that
     p.add_argument("--warmup", type=int, default=40)
-    p.add_argument("--workload", default="full_chunk")
+    p.add_argument("--workload", default=None,
+                   help="time only this workload (default: the full-frame chunk as the headline, plus a "
+                        "record per other workload)")
+    p.add_argument("--sub-steps", type=int, default=10, help="timed steps of each other workload's record")
+    p.add_argument("--sub-warmup", type=int, default=10)
     p.add_argument("--sets", type=int, default=6)
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--qknorm", action="store_true",
@@ -726,10 +735,84 @@ def clip_bench(u, torch, args):
         "dtype": "bf16 in, fp32 accumulate", "data": "synthetic"}), flush=True)
 
 
+SUB_WORKLOADS = ("tiny", "unwindowed", "short_refine", "rolling", "paper_default")
+
+
+def measure_workload(u, torch, wl, n_sets, steps, warmup, qknorm=False):
+    """Time `steps` whole steps of a workload after `warmup` untimed ones, then each kernel of the
+    step on its own; returns the figures of one bench record (attention and append per call,
+    with their roofline fractions, and the step)."""
+    plan = Plan(u, torch, wl, n_sets, qknorm=qknorm)
+    flops, _ = plan.per_step()
+    torch.cuda.synchronize()
+    for _ in range(warmup):
+        plan.step()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        plan.step()
+    t_enq = time.perf_counter() - t0
+    torch.cuda.synchronize()
+    dt = time.perf_counter() - t0
+    ms = dt * 1e3 / steps
+
+    # per-kernel durations: each kernel of the step launched `steps` times back to back (same
+    # calls, same rotating buffer sets) between two HIP events on the stream it runs on
+    extra = {}
+    if wl.name == "rolling":
+        # a stream's attention depends on the ring state its appends left: time the two
+        # kernels of each call between events around each of them instead
+        events = []
+        for _ in range(steps):
+            plan.step(events)
+        torch.cuda.synchronize()
+        app_ms = sum(e0.elapsed_time(e1) for (e0, e1, e2, _, _) in events) / steps
+        att_ms = sum(e1.elapsed_time(e2) for (e0, e1, e2, _, _) in events) / steps
+        nc = len(plan.calls)
+        per_chunk = [sum(events[s * nc + c][1].elapsed_time(events[s * nc + c][2]) for s in range(steps)) * 1e3 / steps
+                     for c in range(nc)]
+        extra["attn_per_chunk_us"] = {"mean": round(sum(per_chunk) / nc, 2), "max": round(max(per_chunk), 2),
+                                      "min": round(min(per_chunk), 2),
+                                      "steady_12_frames_mean": round(sum(per_chunk[11:]) / len(per_chunk[11:]), 2)}
+    else:
+        app_ms, att_ms = plan.time_kernels(steps)
+    per_call_flops = sum(attn_flops(wl.H, C * wl.T, plan.keys(f0, C, W)) * wl.B for (_, f0, C, W) in plan.calls)
+    per_call_bytes = sum(plan.append_bytes(C) for (_, f0, C, W) in plan.calls)
+    ncalls = len(plan.calls)
+    attn_us = att_ms * 1e3 / ncalls
+    app_us = app_ms * 1e3 / ncalls
+    attn_tflops = per_call_flops / (att_ms * 1e-3) / 1e12
+    rope_gbs = per_call_bytes / (app_ms * 1e-3) / 1e9
+    if ncalls > 1:
+        extra["attn_us_per_step"] = round(att_ms * 1e3, 1)
+    app_kernel = "rope_norm_append_kernel" if qknorm else "rope_append_kernel"
+    rec = {
+        "value": round(flops / (ms * 1e-3) / 1e12, 3),
+        "ms_per_step": round(ms, 5),
+        "us_per_step": round(ms * 1e3, 2),
+        "host_enqueue_us_per_step": round(t_enq * 1e6 / steps, 2),
+        "steps": steps, "warmup": warmup,
+        "config": {"workload": wl.name, "batch": wl.B, "heads": wl.H, "head_dim": 128,
+                   "grid": [wl.grid_h, wl.grid_w], "chunk_frames": wl.C, "sink_frames": wl.S,
+                   "window_frames": wl.W, "ring_frames": wl.R, "queries": wl.n_query,
+                   "keys": plan.keys(wl.f0, wl.C, wl.W), "calls_per_step": ncalls,
+                   "buffer_sets": len(plan.sets)},
+        "attn": {"kernel": "window_attn", "us_per_call": round(attn_us, 2), "tflops": round(attn_tflops, 2),
+                 "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+                 "traffic": measured_traffic("window_attn_kernel", wl.name)},
+        "rope_append": {"kernel": app_kernel[:-len("_kernel")], "us_per_call": round(app_us, 2),
+                        "gbs": round(rope_gbs, 1), "frac": round(rope_gbs / PEAK_HBM_GBS, 4),
+                        "traffic": measured_traffic(app_kernel, wl.name)},
+    }
+    rec.update(extra)
+    del plan
+    return rec
+
+
 def main():
     args = parse()
     if args.summarize_profile:
-        summarize_profile(args.summarize_profile, args.workload, args.qknorm)
+        summarize_profile(args.summarize_profile, args.workload or "full_chunk", args.qknorm)
         return
     if args.summarize_trace:
         summarize_trace(args.summarize_trace, args.trace_name or "trace", args.trace_command or "")
@@ -767,66 +850,38 @@ def main():
     if args.oproj:
         oproj_bench(u, torch, args)
         return
-    wl = synth.WORKLOADS[args.workload]
-    plan = Plan(u, torch, wl, args.sets, qknorm=args.qknorm)
-    flops, rbytes = plan.per_step()
-    torch.cuda.synchronize()
-
-    for _ in range(args.warmup):
-        plan.step()
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        plan.step()
-    t_enq = time.perf_counter() - t0
-    torch.cuda.synchronize()
-    dt = time.perf_counter() - t0
-    ms = dt * 1e3 / args.steps
-
-    # per-kernel durations: each kernel of the step launched `steps` times back to back (same
-    # calls, same rotating buffer sets) between two HIP events on the stream it runs on
-    if wl.name == "rolling":
-        # a stream's attention depends on the ring state its appends left: time the two
-        # kernels of each call between events around each of them instead
-        events = []
-        for _ in range(args.steps):
-            plan.step(events)
-        torch.cuda.synchronize()
-        app_ms = sum(e0.elapsed_time(e1) for (e0, e1, e2, _, _) in events) / args.steps
-        att_ms = sum(e1.elapsed_time(e2) for (e0, e1, e2, _, _) in events) / args.steps
-    else:
-        app_ms, att_ms = plan.time_kernels(args.steps)
-    per_call_flops = sum(attn_flops(wl.H, C * wl.T, plan.keys(f0, C, W)) * wl.B for (_, f0, C, W) in plan.calls)
-    per_call_bytes = sum(plan.append_bytes(C) for (_, f0, C, W) in plan.calls)
-    ncalls = len(plan.calls)
-    attn_us = att_ms * 1e3 / ncalls
-    app_us = app_ms * 1e3 / ncalls
-    attn_tflops = per_call_flops / (att_ms * 1e-3) / 1e12
-    rope_gbs = per_call_bytes / (app_ms * 1e-3) / 1e9
-
-    value = flops / (ms * 1e-3) / 1e12
+    headline = args.workload or "full_chunk"
+    wl = synth.WORKLOADS[headline]
+    m = measure_workload(u, torch, wl, args.sets, args.steps, args.warmup, qknorm=args.qknorm)
     app_kernel = "rope_norm_append_kernel" if args.qknorm else "rope_append_kernel"
     res = {
-        "metric": METRIC, "value": round(value, 3), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
-        "warmup": args.warmup, "ms_per_step": round(ms, 5), "higher_is_better": True, "scaling": "weak",
+        "metric": METRIC, "value": m["value"], "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": m["ms_per_step"], "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": wl.name, "batch": wl.B, "heads": wl.H, "head_dim": 128,
-                   "grid": [wl.grid_h, wl.grid_w], "chunk_frames": wl.C, "sink_frames": wl.S,
-                   "window_frames": wl.W, "ring_frames": wl.R, "queries": wl.n_query,
-                   "keys": plan.keys(wl.f0, wl.C, wl.W), "calls_per_step": len(plan.calls),
-                   "buffer_sets": len(plan.sets), "qk_rmsnorm": bool(args.qknorm), "parallelism": "single GPU"},
-        "us_per_step": round(ms * 1e3, 2),
-        "host_enqueue_us_per_step": round(t_enq * 1e6 / args.steps, 2),
-        "attn": {"kernel": "window_attn", "us_per_call": round(attn_us, 2), "tflops": round(attn_tflops, 2)},
-        "rope_append": {"kernel": app_kernel[:-len("_kernel")], "us_per_call": round(app_us, 2),
-                        "gbs": round(rope_gbs, 1)},
-        "roofline": {"bound": "mfma", "achieved": round(attn_tflops, 2), "peak": PEAK_BF16_TFLOPS,
-                     "unit": "TFLOP/s", "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+        "config": dict(m["config"], qk_rmsnorm=bool(args.qknorm), parallelism="single GPU"),
+        "us_per_step": m["us_per_step"],
+        "host_enqueue_us_per_step": m["host_enqueue_us_per_step"],
+        "attn": m["attn"],
+        "rope_append": m["rope_append"],
+        "roofline": {"bound": "mfma", "achieved": m["attn"]["tflops"], "peak": PEAK_BF16_TFLOPS,
+                     "unit": "TFLOP/s", "frac": m["attn"]["frac"],
                      "traffic": measured_traffic("window_attn_kernel", wl.name)},
-        "rope_roofline": {"bound": "hbm", "achieved": round(rope_gbs, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
-                          "frac": round(rope_gbs / PEAK_HBM_GBS, 4),
+        "rope_roofline": {"bound": "hbm", "achieved": m["rope_append"]["gbs"], "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                          "frac": m["rope_append"]["frac"],
                           "traffic": measured_traffic(app_kernel, wl.name)},
     }
+    for k in ("attn_per_chunk_us", "attn_us_per_step"):
+        if k in m:
+            res[k] = m[k]
+    # every other workload of the benchmark, measured in the same run (same box, same clock
+    # conditions), with fewer steps: each a full step of its own shape
+    if args.workload is None and not args.qknorm and args.sub_steps > 0:
+        res["workloads"] = {}
+        for name in SUB_WORKLOADS:
+            sub = measure_workload(u, torch, synth.WORKLOADS[name], args.sets, args.sub_steps, args.sub_warmup)
+            sub.pop("config")
+            res["workloads"][name] = sub
+            torch.cuda.empty_cache()
     if not args.no_cpu_baseline:
         res["cpu_baseline"] = cpu_baseline(wl, args.cpu_queries)
     print(json.dumps(res), flush=True)

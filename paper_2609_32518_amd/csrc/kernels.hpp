@@ -39,6 +39,12 @@ constexpr int kNormMaxHeads = 32;
 
 hipError_t launch_rope_append(const RopeAppendArgs& a, hipStream_t stream);
 
+// Attention tiling: 256 queries per work-group (8 waves x 32), 64 keys per tile, and at most
+// one work-group per compute unit (256 on MI355X) in the balanced schedule.
+constexpr int kAttnBlockQ = 256;
+constexpr int kAttnBlockK = 64;
+constexpr int kAttnMaxGroups = 256;
+
 // Attention of a chunk's queries over the retained cache rows.
 struct AttnArgs {
   const uint16_t* q;       // bf16 [B, N, H, 128] contiguous (rotated queries)
@@ -46,8 +52,8 @@ struct AttnArgs {
   const uint16_t* v_cache;
   uint16_t* out;           // bf16 [B, N, H, 128]
   float* lse;              // [B, H, N] or null
-  float* part_o;           // balanced schedule: partial outputs [groups, 2, 128, 128] fp32
-  float* part_ml;          // ... and their (exponent offset, row sum) [groups, 2, 128, 2]; null
+  float* part_o;           // balanced schedule: partial outputs [groups, 2, 256, 128] fp32
+  float* part_ml;          // ... and their (exponent offset, row sum) [groups, 2, 256, 2]; null
                            // when groups equals the number of query tiles (no partials)
   int32_t B, N, H, slots;
   int32_t n_keys;          // retained keys
@@ -78,7 +84,12 @@ hipError_t launch_widen_f64(const float* x, double* y, int64_t n, hipStream_t st
 hipError_t launch_narrow_f32(const double* x, float* y, int64_t n, hipStream_t stream);
 
 AttnPlan attn_plan(int32_t B, int32_t H, int32_t N, int32_t n_keys);
-size_t attn_workspace_bytes(int32_t groups);
+
+// Scratch of a balanced launch: two partial-output slots of 256 rows x 128 fp32 per
+// work-group, then their (exponent offset, row sum) pairs.
+constexpr size_t attn_workspace_bytes(int32_t groups) {
+  return size_t(groups) * 2 * kAttnBlockQ * (kHeadDim + 2) * sizeof(float);
+}
 hipError_t launch_window_attn(const AttnArgs& a, hipStream_t stream);
 
 }  // namespace unstep
