@@ -211,6 +211,25 @@ int unstep_window_attn(const unstep_cache* c, int32_t start_frame, int32_t n_fra
                        float softmax_scale, void* workspace, size_t workspace_bytes,
                        void* hip_stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture, serving
+ * loops, harnesses that forbid hipMalloc): unstep_window_attn with the split-key scratch taken
+ * from a static device array inside the library instead of a workspace argument.  The array
+ * holds the partials of the largest split the library plans (256 work-groups: 68,157,440
+ * bytes); each device the library runs on gets its own copy, which it holds until the process
+ * ends.  The first call on a device looks up the array's device address (hipGetSymbolAddress);
+ * no call allocates or frees device memory, enqueues a memset or synchronises.  The array of
+ * the current device is used, so hip_stream must belong to the current device.  Every call on
+ * a device shares that device's array: calls that may overlap on one device (different streams
+ * without ordering between them) race on it and must not be issued; calls on one stream, or
+ * ordered by events, are safe.  Nothing in it needs to start at zero: each launch writes every
+ * partial it reads.  Results equal those of unstep_window_attn given a workspace of at least
+ * unstep_attn_workspace_size bytes, bit for bit.  Errors: those of unstep_window_attn, plus
+ * E_SHAPE if a split ever needed more than the static array holds, E_HIP if the address lookup
+ * fails. */
+int unstep_window_attn_noalloc(const unstep_cache* c, int32_t start_frame, int32_t n_frames,
+                               int32_t window_frames, const void* q_rot, void* out, float* lse,
+                               float softmax_scale, void* hip_stream);
+
 /* ---------------------------------------------------------------------------------
  * One whole chunk step: unstep_kv_append followed by unstep_window_attn on the same
  * stream (q must not be NULL).  All checks of both halves run before anything is

@@ -63,6 +63,7 @@ SIGNATURES = {
     "unstep_renoise": (ctypes.c_int, [_vp, _vp, _f64, _vp, _i64, _vp]),
     "unstep_emit": (ctypes.c_int, [_vp, _vp, _f64, _vp, _i64, _vp]),
     "unstep_window_attn": (ctypes.c_int, [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _f32, _vp, _sz, _vp]),
+    "unstep_window_attn_noalloc": (ctypes.c_int, [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _f32, _vp]),
     "unstep_step": (ctypes.c_int, [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _i64, _i64, _vp, _vp, _vp, _vp, _vp,
                                    _f32, _vp, _sz, _vp]),
 }
@@ -325,6 +326,19 @@ class Cache:
                                       out.data_ptr(), _ptr(lse), softmax_scale, _ptr(workspace), ws_bytes,
                                       _stream(stream)))
         _used_on(stream, out, workspace)
+        return out
+
+    def unstep_window_attn_noalloc(self, start_frame: int, n_frames: int, window_frames: int, q_rot: torch.Tensor,
+                                   out: torch.Tensor, lse: Optional[torch.Tensor] = None, softmax_scale: float = 0.0,
+                                   stream=None) -> torch.Tensor:
+        """unstep_window_attn with the split-key scratch in the library's static device array (no
+        workspace, no allocation in the library; the caller passes the output).  Calls that may
+        overlap on one device race on that array."""
+        _need(q_rot, "q_rot", (self.B, n_frames * self.T, self.H, HEAD_DIM), torch.bfloat16, self.device)
+        _need(out, "out", (self.B, n_frames * self.T, self.H, HEAD_DIM), torch.bfloat16, self.device)
+        self._lse(lse, n_frames)
+        _check(lib.unstep_window_attn_noalloc(self.handle, start_frame, n_frames, window_frames, q_rot.data_ptr(),
+                                              out.data_ptr(), _ptr(lse), softmax_scale, _stream(stream)))
         return out
 
     def unstep_step(self, start_frame: int, n_frames: int, window_frames: int, q: torch.Tensor, k: torch.Tensor,

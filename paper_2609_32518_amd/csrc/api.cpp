@@ -330,6 +330,35 @@ int unstep_window_attn(const unstep_cache* c, int32_t start_frame, int32_t n_fra
   });
 }
 
+int unstep_window_attn_noalloc(const unstep_cache* c, int32_t start_frame, int32_t n_frames, int32_t window_frames,
+                               const void* q_rot, void* out, float* lse, float softmax_scale, void* hip_stream) {
+  return unstep::guarded("unstep_window_attn_noalloc", [&]() -> int {
+    const char* where = "unstep_window_attn_noalloc";
+    if (!c) return fail(UNSTEP_E_NULL, "%s: cache handle is NULL", where);
+    unstep::AttnArgs a;
+    int rc = plan_attn(c, c->idx, start_frame, n_frames, window_frames, q_rot, out, lse, softmax_scale, nullptr, 0,
+                       &a, where);
+    if (rc != UNSTEP_OK) return rc;
+    const unstep::AttnPlan plan = unstep::attn_plan(a.B, a.H, a.N, a.n_keys);
+    if (plan.workspace > 0) {
+      // the split-key partials go to the library's static scratch of the current device
+      if (plan.workspace > unstep::kAttnMaxWorkspace)
+        return fail(UNSTEP_E_SHAPE, "%s: the split needs %zu bytes of scratch, more than the static %zu", where,
+                    plan.workspace, unstep::kAttnMaxWorkspace);
+      void* scratch = nullptr;
+      size_t bytes = 0;
+      hipError_t e = unstep::static_attn_scratch(&scratch, &bytes);
+      if (e != hipSuccess) return fail(UNSTEP_E_HIP, "%s: scratch lookup: %s", where, hipGetErrorString(e));
+      a.groups = plan.groups;
+      a.part_o = static_cast<float*>(scratch);
+      a.part_ml = static_cast<float*>(scratch) + plan.part_o_floats;
+    }
+    hipError_t e = unstep::launch_window_attn(a, static_cast<hipStream_t>(hip_stream));
+    if (e != hipSuccess) return fail(UNSTEP_E_HIP, "%s: %s", where, hipGetErrorString(e));
+    return ok();
+  });
+}
+
 int unstep_step(unstep_cache* c, int32_t start_frame, int32_t n_frames, int32_t window_frames, const void* q,
                 const void* k, const void* v, int64_t tok_stride, int64_t head_stride, const float* cos_t,
                 const float* sin_t, void* q_rot, void* out, float* lse, float softmax_scale, void* workspace,

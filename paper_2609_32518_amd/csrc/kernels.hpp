@@ -90,6 +90,13 @@ AttnPlan attn_plan(int32_t B, int32_t H, int32_t N, int32_t n_keys);
 constexpr size_t attn_workspace_bytes(int32_t groups) {
   return size_t(groups) * 2 * kAttnBlockQ * (kHeadDim + 2) * sizeof(float);
 }
+// The most any launch needs (kAttnMaxGroups work-groups).
+constexpr size_t kAttnMaxWorkspace = attn_workspace_bytes(kAttnMaxGroups);
+
 hipError_t launch_window_attn(const AttnArgs& a, hipStream_t stream);
+
+// The allocation-free entry point's scratch on the current device: a static device array of
+// kAttnMaxWorkspace bytes whose device address is looked up once per device and kept.
+hipError_t static_attn_scratch(void** ptr, size_t* bytes);
 
 }  // namespace unstep

@@ -47,6 +47,7 @@
 #include <algorithm>
 #include <cfloat>
 #include <climits>
+#include <mutex>
 
 #include "kernels.hpp"
 
@@ -659,6 +660,34 @@ hipError_t launch_window_attn(const AttnArgs& a, hipStream_t stream) {
   const int64_t qtiles = int64_t(a.B) * a.H * ((a.N + kBlockQ - 1) / kBlockQ);
   hipLaunchKernelGGL(attn_combine_kernel, dim3(unsigned(qtiles * (kBlockQ / kCombineRows))), dim3(256), 0, stream, a);
   return hipGetLastError();
+}
+
+// Scratch of the allocation-free entry point (unstep_window_attn_noalloc): room for the
+// partials of the largest balanced launch, one copy per device that the library runs on,
+// held until the process ends.  Host code never passes the array's name to a kernel (on
+// the host it names a stand-in, not device memory): it looks up the device address once per
+// device with hipGetSymbolAddress and passes that.
+static __device__ __align__(256) uint8_t scratch[kAttnMaxWorkspace];
+
+hipError_t static_attn_scratch(void** ptr, size_t* bytes) {
+  constexpr int kMaxDevices = 64;
+  static std::mutex mu;
+  static void* addr[kMaxDevices] = {};
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p) return hipErrorInvalidSymbol;
+    addr[dev] = p;
+  }
+  *ptr = addr[dev];
+  *bytes = kAttnMaxWorkspace;
+  return hipSuccess;
 }
 
 }  // namespace unstep

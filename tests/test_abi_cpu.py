@@ -470,3 +470,19 @@ def test_huge_frame_requests_fail_fast_without_allocating():
         assert _frame_map(h, 6) == ([0, 1, 2, -1, -1, -1], 2)
     finally:
         u.lib.unstep_cache_destroy(h)
+
+
+def test_noalloc_attention_checks_arguments_before_any_device_work():
+    rc, h = _handle(1, 2, 4, 6, 0, 9)
+    assert rc == u.OK
+    try:
+        f = u.lib.unstep_window_attn_noalloc
+        assert f(None, 0, 1, 0, FAKE[2], FAKE[3], None, 0.0, None) == u.E_NULL
+        assert f(h, 0, 1, 0, None, FAKE[3], None, 0.0, None) == u.E_NULL
+        assert f(h, 0, 1, 0, FAKE[2], FAKE[3], None, 0.0, None) == u.E_STATE      # nothing appended
+        assert u.lib.unstep_cache_advance(h, 0, 3) == u.OK
+        assert f(h, 0, 3, 0, FAKE[2] + 8, FAKE[3], None, 0.0, None) == u.E_ALIGN
+        assert f(h, 0, 3, 0, FAKE[2], FAKE[3], FAKE[4] + 2, 0.0, None) == u.E_ALIGN     # lse
+        assert f(h, 5, 3, 0, FAKE[2], FAKE[3], None, 0.0, None) == u.E_STATE
+    finally:
+        u.lib.unstep_cache_destroy(h)
