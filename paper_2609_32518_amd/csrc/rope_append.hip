@@ -19,6 +19,7 @@
 #include <hip/hip_runtime.h>
 
 #include "kernels.hpp"
+#include "seg_table.hpp"
 
 namespace unstep {
 namespace {
@@ -65,7 +66,7 @@ __global__ __launch_bounds__(kThreads) void rope_append_kernel(RopeAppendArgs a)
   const int32_t fi = blockIdx.y;                         // frame within the chunk
   const int32_t b = blockIdx.z;
   const int32_t f = a.f0 + fi;
-  const int32_t slot = f < a.S ? f : a.S + (f - a.S) % a.R;
+  const int32_t slot = frame_slot(f, a.S, a.R);
   const int64_t n = int64_t(fi) * a.T + t;
   const int64_t N = int64_t(a.C) * a.T;
 
@@ -148,7 +149,7 @@ __global__ __launch_bounds__(kThreads) void rope_norm_append_kernel(RopeAppendAr
   const int b = blockIdx.y;
   const int32_t fi = n / a.T, t = n - fi * a.T;
   const int32_t f = a.f0 + fi;
-  const int32_t slot = f < a.S ? f : a.S + (f - a.S) % a.R;
+  const int32_t slot = frame_slot(f, a.S, a.R);
   const int32_t pieces = a.H * kPieces;
   const int np = (pieces - lane + 63) / 64;                               // this lane's pieces
 

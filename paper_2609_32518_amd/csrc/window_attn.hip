@@ -50,6 +50,7 @@
 #include <mutex>
 
 #include "kernels.hpp"
+#include "seg_table.hpp"
 
 namespace unstep {
 namespace {
@@ -83,28 +84,6 @@ typedef __attribute__((address_space(3))) void lds_void_t;
 // reads (16 lanes = 16 consecutive rows at one logical slot) and the transposing V reads
 // (per half-wave 4 consecutive rows x 4 consecutive slots).
 __device__ __forceinline__ int swz(int row) { return ((row & 3) << 2) | ((row >> 2) & 3); }
-
-// Physical cache row of a logical key index: up to four runs of consecutive rows, the
-// first starting at logical index 0.
-struct SegTable {
-  int32_t l1, l2, l3;          // logical start of runs 1..3 (INT32_MAX when absent)
-  int32_t r0, r1, r2, r3;      // physical row of each run's first key
-  __device__ __forceinline__ int32_t row(int32_t key) const {
-    int32_t r = r0 + key;
-    r = key >= l1 ? r1 + (key - l1) : r;
-    r = key >= l2 ? r2 + (key - l2) : r;
-    r = key >= l3 ? r3 + (key - l3) : r;
-    return r;
-  }
-  // Logical start of the run after the one holding key (INT32_MAX for the last run).
-  __device__ __forceinline__ int32_t run_end(int32_t key) const {
-    return key < l1 ? l1 : key < l2 ? l2 : key < l3 ? l3 : INT32_MAX;
-  }
-  // Logical start of the run holding key.
-  __device__ __forceinline__ int32_t run_start(int32_t key) const {
-    return key >= l3 ? l3 : key >= l2 ? l2 : key >= l1 ? l1 : 0;
-  }
-};
 
 __device__ __forceinline__ bf16x8_t as_bf16x8(u32x4_t u) { return __builtin_bit_cast(bf16x8_t, u); }
 
@@ -141,10 +120,8 @@ struct Walk {
   int32_t k_begin, k_end;      // logical key range
   int32_t n;                   // tiles in the range
   int half;
-  int lrow;                    // loader: tile row of this lane in its first load (+4)
-  // loader cursors of walks over several runs, one for K tiles and one for V tiles: a tile
-  // whose keys [kt0, kt0 + 64) lie in [lo, hi) maps key kt0 to row kt0 + delta
-  int32_t kc_lo, kc_hi, kc_delta, vc_lo, vc_hi, vc_delta;
+  int lrow;                    // loader: tile row of this lane in its first load (+4 in the second)
+  RowCursor kc, vc;            // loader cursors of walks over several runs (K tiles, V tiles)
   int lpiece[2];               // loader: byte offset of this lane's logical 16-byte piece
   uint32_t lds_k, lds_v;       // LDS address of ring slot 0's K tile and V tile (uniform)
   uint32_t koff[8];            // LDS address of the K fragment for d-step 0..7 in slot 0
@@ -154,35 +131,19 @@ struct Walk {
 
 // Direct-to-LDS load of 8 rows (this wave's share) of the 64-key tile starting at logical
 // key kt0 into the tile at LDS address dst: lane l of instruction i lands in row lrow + 4 i,
-// physical slot l & 15, and so fetches logical piece (l & 15) ^ swz(row).  Keys past the
-// range read the range's last key (finite values; their scores are masked to -inf).
-// kOneRun: the walk's whole range lies in the segment table's first run (a cache that has not
-// wrapped and holds no separate sinks), so rows follow keys with no table lookup.  Otherwise a
-// cursor (lo, hi, delta) per operand remembers the run of the last tile it mapped: a tile
-// inside it costs two scalar compares, and only a tile that crosses a run boundary or the
-// range's end looks rows up per lane and moves the cursor to the run of the tile after it.
-// Both keep the scalar work of the V phase, which shares the wave's issue slots with its
-// softmax, small.
+// lrow = 8 wave + (l >> 4), physical slot l & 15, and so fetches logical piece
+// (l & 15) ^ swz(row).  The rows come from tile_rows (the walk's segment table and its
+// cursor for this operand); keys past the range read the range's last key (finite values;
+// their scores are masked to -inf).  The scalar work of the lookup shares the V-phase wave's
+// issue slots with its softmax, which is why a range inside one run takes the lookup-free path
+// and other walks keep a cursor per operand.
 // Written as inline assembly: M0 holds the wave's LDS destination, the lane's 16 bytes land
 // at M0 + 16 l.
 template <bool kOneRun>
-__device__ __forceinline__ void load_rows(uint32_t dst, const uint8_t* base, const Walk& w, int32_t& c_lo,
-                                          int32_t& c_hi, int32_t& c_delta, int wave, int32_t kt0) {
+__device__ __forceinline__ void load_rows(uint32_t dst, const uint8_t* base, const Walk& w, RowCursor& cur, int wave,
+                                          int32_t kt0) {
   int32_t rows[2];
-  if (kOneRun) {                 // the whole range lies in the first run: rows follow keys
-#pragma unroll
-    for (int i = 0; i < 2; ++i) rows[i] = min(kt0 + w.lrow + 4 * i, w.k_end - 1) + w.seg.r0;
-  } else if (kt0 >= c_lo && kt0 + kBlockK <= c_hi) {     // whole tile inside the cursor's run
-    rows[0] = kt0 + c_delta + w.lrow;
-    rows[1] = rows[0] + 4;
-  } else {                       // crosses a run boundary or the range's end: per-lane lookup
-#pragma unroll
-    for (int i = 0; i < 2; ++i) rows[i] = w.seg.row(min(kt0 + w.lrow + 4 * i, w.k_end - 1));
-    const int32_t nx = kt0 + kBlockK;       // move the cursor to the run of the next tile
-    c_lo = w.seg.run_start(nx);
-    c_hi = min(w.seg.run_end(nx), w.k_end);
-    c_delta = w.seg.row(nx) - nx;
-  }
+  tile_rows<kOneRun, kBlockK, 2, 4>(w.seg, w.k_end, cur, kt0, w.lrow, rows);
 #pragma unroll
   for (int i = 0; i < 2; ++i) {
     const uint32_t off = uint32_t(rows[i]) * kRowBytes + w.lpiece[i];
@@ -197,10 +158,8 @@ __device__ __forceinline__ void load_rows(uint32_t dst, const uint8_t* base, con
 template <bool kOneRun>
 __device__ __forceinline__ void load_stage(int slot, Walk& w, int wave, int32_t t) {
   const int32_t tk = min(t, w.n - 1), tv = max(t - 1, 0);
-  load_rows<kOneRun>(w.lds_k + slot * kTileBytes, w.kbase, w, w.kc_lo, w.kc_hi, w.kc_delta, wave,
-                     w.k_begin + tk * kBlockK);
-  load_rows<kOneRun>(w.lds_v + slot * kTileBytes, w.vbase, w, w.vc_lo, w.vc_hi, w.vc_delta, wave,
-                     w.k_begin + tv * kBlockK);
+  load_rows<kOneRun>(w.lds_k + slot * kTileBytes, w.kbase, w, w.kc, wave, w.k_begin + tk * kBlockK);
+  load_rows<kOneRun>(w.lds_v + slot * kTileBytes, w.vbase, w, w.vc, wave, w.k_begin + tv * kBlockK);
 }
 
 // Register state of one wave.
@@ -282,7 +241,7 @@ __device__ __forceinline__ void v_phase(Acc& a, int32_t t, Walk& w, int wave) {
   // this wave's share of stage t + 3 (K tile t + 3, V tile t + 2) into the slot that held
   // stage t - 1
   const bool load = t + kAhead <= w.n;
-  if (load) load_rows<kOneRun>(w.lds_k + kLoadSlot * kTileBytes, w.kbase, w, w.kc_lo, w.kc_hi, w.kc_delta, wave, w.k_begin + min(t + kAhead, w.n - 1) * kBlockK);
+  if (load) load_rows<kOneRun>(w.lds_k + kLoadSlot * kTileBytes, w.kbase, w, w.kc, wave, w.k_begin + min(t + kAhead, w.n - 1) * kBlockK);
   const int32_t kt0 = w.k_begin + t * kBlockK;
   if (kt0 + kBlockK > w.k_end) {
 #pragma unroll
@@ -294,7 +253,7 @@ __device__ __forceinline__ void v_phase(Acc& a, int32_t t, Walk& w, int wave) {
   if (kMode == 2) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) a.mx = fmaxf(a.mx, fmaxf(a.s[0][i], a.s[1][i]));
-    if (load) load_rows<kOneRun>(w.lds_v + kLoadSlot * kTileBytes, w.vbase, w, w.vc_lo, w.vc_hi, w.vc_delta, wave, w.k_begin + (t + kAhead - 1) * kBlockK);
+    if (load) load_rows<kOneRun>(w.lds_v + kLoadSlot * kTileBytes, w.vbase, w, w.vc, wave, w.k_begin + (t + kAhead - 1) * kBlockK);
     return;
   }
   if (kMode == 0 && t == 0) {
@@ -317,7 +276,7 @@ __device__ __forceinline__ void v_phase(Acc& a, int32_t t, Walk& w, int wave) {
       a.p[kb][i >> 3][(i & 7) + 1] = (__bf16)e1;
     }
   a.l += acc0 + acc1;
-  if (load) load_rows<kOneRun>(w.lds_v + kLoadSlot * kTileBytes, w.vbase, w, w.vc_lo, w.vc_hi, w.vc_delta, wave, w.k_begin + (t + kAhead - 1) * kBlockK);
+  if (load) load_rows<kOneRun>(w.lds_v + kLoadSlot * kTileBytes, w.vbase, w, w.vc, wave, w.k_begin + (t + kAhead - 1) * kBlockK);
 }
 
 // Tile t of the walk, with stage t in ring slot kSlot: the M phase of tile t, the stage
@@ -340,9 +299,9 @@ __device__ __forceinline__ void step(Acc& a, Walk& w, const bf16x8_t (&qf)[8], i
   if (kIdle) {
     // a wave with no query of the tile: only its share of the loads, in the same order
     if (t < w.n && t + kAhead <= w.n) {
-      load_rows<kOneRun>(w.lds_k + kLoadSlot * kTileBytes, w.kbase, w, w.kc_lo, w.kc_hi, w.kc_delta, wave,
+      load_rows<kOneRun>(w.lds_k + kLoadSlot * kTileBytes, w.kbase, w, w.kc, wave,
                          w.k_begin + min(t + kAhead, w.n - 1) * kBlockK);
-      load_rows<kOneRun>(w.lds_v + kLoadSlot * kTileBytes, w.vbase, w, w.vc_lo, w.vc_hi, w.vc_delta, wave,
+      load_rows<kOneRun>(w.lds_v + kLoadSlot * kTileBytes, w.vbase, w, w.vc, wave,
                          w.k_begin + (t + kAhead - 1) * kBlockK);
     }
   } else if (t < w.n) {
@@ -371,9 +330,8 @@ __device__ __forceinline__ void walk(Acc& a, Walk& w, const bf16x8_t (&qf)[8], i
   __builtin_amdgcn_s_waitcnt(0);
   barrier();                                   // the ring is free
   if (!kOneRun) {                              // loader cursors at the range's first key
-    w.kc_lo = w.vc_lo = w.seg.run_start(w.k_begin);
-    w.kc_hi = w.vc_hi = min(w.seg.run_end(w.k_begin), w.k_end);
-    w.kc_delta = w.vc_delta = w.seg.row(w.k_begin) - w.k_begin;
+    cursor_at(w.seg, w.k_end, w.k_begin, w.kc);
+    w.vc = w.kc;
   }
 #pragma unroll
   for (int t = 0; t < kAhead; ++t)
@@ -389,15 +347,6 @@ __device__ __forceinline__ void walk(Acc& a, Walk& w, const bf16x8_t (&qf)[8], i
   }
   if (group == 0) barrier();                   // group A idles in the last phase
 }
-
-// Unit bookkeeping of the balanced schedule: unit u = (query tile t, key tile k) =
-// t * Tk + k; work-group g owns units [start(g), start(g + 1)), start(g) = floor(g U / G).
-struct Schedule {
-  int64_t U, G;
-  int32_t Tk;
-  __device__ __forceinline__ int64_t start(int64_t g) const { return g * U / G; }
-  __device__ __forceinline__ int64_t owner(int64_t u) const { return ((u + 1) * G - 1) / U; }
-};
 
 __device__ __forceinline__ Schedule make_schedule(const AttnArgs& a, int32_t* qtiles_out) {
   const int32_t qtiles = (a.N + kBlockQ - 1) / kBlockQ;
@@ -469,13 +418,11 @@ __global__ __launch_bounds__(kThreads) void window_attn_kernel(AttnArgs a) {
   // tile, so work-groups stream the same keys at about the same time (shared L2).
   const int64_t u_begin = sc.start(g);
   for (int64_t u_hi = sc.start(int64_t(g) + 1); u_hi > u_begin;) {
-    const int64_t t = (u_hi - 1) / sc.Tk;
-    const int64_t u_lo = max<int64_t>(u_begin, t * sc.Tk);
-    const int32_t k0 = int32_t(u_lo - t * sc.Tk);
-    const int32_t k1 = int32_t(u_hi - t * sc.Tk);
-    const int slot = u_lo == u_begin ? 0 : 1;
-    const bool full = k0 == 0 && k1 == sc.Tk;
-    u_hi = u_lo;
+    const Segment sg = take_segment(sc, u_begin, u_hi);
+    const int64_t t = sg.t;
+    const int32_t k0 = sg.k0, k1 = sg.k1;
+    const int slot = sg.slot;
+    const bool full = sg.full;
 
     const int32_t qt = int32_t(t % qtiles);
     const int32_t bh_idx = int32_t(t / qtiles);      // b * H + h
