@@ -21,7 +21,10 @@ buffer sets (cache + inputs + outputs) are rotated so that consecutive steps do 
 find their data in the 256 MB Infinity Cache.  W warm-up steps, then K timed steps
 between device synchronisations; per-kernel durations come from HIP events recorded
 on the stream the kernels run on: each kernel of the step launched for the same calls
-back to back between two events.
+back to back between two events after an untimed pass (which loads the kernels); the
+short append and copy kernels are enqueued behind a device-side spin so that the events
+bracket GPU time only, with no host enqueue gap.  A plain three-buffer copy of the append pass's inputs (unstep_copy3) is timed
+the same way as its bandwidth reference (`append_copy_baseline`).
 
 Prints one JSON line.
 """
@@ -194,26 +197,100 @@ class Plan:
             return call_set
         return self.step_idx % len(self.sets)
 
+    def behind_wait(self, enqueue, steps, spin=True):
+        """Run enqueue() `steps` times between two HIP events on the current stream after one
+        untimed pass (which also loads the kernels).  spin: enqueue it all behind a device-side
+        spin long enough for the host to enqueue every launch first, so that the events bracket
+        GPU time only, with no host enqueue gap; for kernels short against the binding's host
+        time.  Kernels much longer than it (attention) run without the spin: a spin leaves the
+        power-limited chip in a different clock state than the step loop does.  Returns ms per
+        pass."""
+        torch = self.torch
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        enqueue()                                    # untimed pass: loads the kernels, sizes the wait
+        t_host = time.perf_counter() - t0
+        if spin:
+            torch.cuda.synchronize()
+            wait_s = min(1.0, 2.0 * t_host * steps + 2e-3)
+            torch.cuda._sleep(int(wait_s * 2.5e9))  # spin counted in shader cycles (<= 2.4 GHz)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            enqueue()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps
+
     def time_kernels(self, steps):
         """Average per-step time (ms) of the appends and of the attention calls, each launched
-        for `steps` steps back to back between two HIP events on the current stream."""
-        torch, wl = self.torch, self.wl
+        for `steps` steps back to back (behind_wait)."""
         out = []
         for which in ("append", "attn"):
             self.step_idx = 0
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            for _ in range(steps):
-                self.step(only=which)
-            e1.record()
-            torch.cuda.synchronize()
-            out.append(e0.elapsed_time(e1) / steps)
+            out.append(self.behind_wait(lambda: self.step(only=which), steps, spin=which == "append"))
         return out
 
-    def step(self, events=None, only=None):
-        """Enqueue one step.  With `events` (list), record (append_start, append_end=attn_start,
-        attn_end) events around each call's two kernels."""
+    def time_rolling(self, steps):
+        """The rolling stream's kernels, each kind back to back: the appends of the 60 chunks on a
+        fresh ring (one event pair around each step's appends, behind the spin: they are short),
+        then the attention calls with an event pair around each (its key range grows over the
+        stream), the host index advanced between them without device work
+        (unstep_cache_advance) so that each call attends the key range its chunk has; the
+        timing does not depend on what the ring holds.  Returns (append ms per step, attention
+        ms per call over all timed steps in chunk order)."""
         torch, wl = self.torch, self.wl
+        att = []
+
+        def one_step(which):
+            s = self.sets[self.step_idx % len(self.sets)]
+            cache = self.u.Cache(wl.B, wl.H, wl.grid_h, wl.grid_w, wl.S, wl.R, k_cache=s["cache"].k,
+                                 v_cache=s["cache"].v)
+            for (_, f0, C, W) in self.calls:
+                N = C * wl.T
+                if which == "append":
+                    cos_t, sin_t = self.tables.get(f0, C, wl.grid_h, wl.grid_w)
+                    self._append(dict(s, cache=cache), f0, C, s["q"][:, :N], s["k"][:, :N], s["v"][:, :N],
+                                 cos_t, sin_t, s["q_rot"][:, :N])
+                else:
+                    cache.advance(f0, C)
+                    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+                    a.record()
+                    cache.unstep_window_attn(f0, C, W, s["q_rot"][:, :N], out=s["out"][:, :N],
+                                             workspace=self.ws.get(self.step_idx % len(self.sets)))
+                    b.record()
+                    att.append((a, b))
+            self.step_idx += 1
+
+        self.step_idx = 0
+        app_ms = self.behind_wait(lambda: one_step("append"), steps, spin=True)
+        self.step_idx = 0
+        self.behind_wait(lambda: one_step("attn"), steps, spin=False)
+        return app_ms, [a.elapsed_time(b) for (a, b) in att[len(self.calls):]]    # the untimed pass dropped
+
+    def time_copy_baseline(self, steps):
+        """Average per-step time (ms) of a plain three-buffer copy of each call's q, k, v (the
+        append pass's inputs) into three other buffers, one launch per call with the pass's
+        access pattern (unstep_copy3), over the same rotating buffer sets (behind_wait)."""
+        torch, wl = self.torch, self.wl
+        if not hasattr(self, "copy_dst"):
+            self.copy_dst = [tuple(torch.empty_like(s["q"]) for _ in range(3)) for s in self.sets]
+
+        def one_step():
+            for (cs, f0, C, W) in self.calls:
+                si = self._set_for(cs)
+                s, d = self.sets[si], self.copy_dst[si]
+                N = C * wl.T
+                self.u.unstep_copy3(s["q"][:, :N], s["k"][:, :N], s["v"][:, :N], d[0][:, :N], d[1][:, :N],
+                                    d[2][:, :N])
+            self.step_idx += 1
+
+        self.step_idx = 0
+        return self.behind_wait(one_step, steps, spin=True)
+
+    def step(self, only=None):
+        """Enqueue one step (only="append" / "attn": just that kernel of each call)."""
+        wl = self.wl
         if wl.name == "rolling":
             si = self.step_idx % len(self.sets)
             s = self.sets[si]
@@ -231,19 +308,11 @@ class Plan:
                 self._append(s, f0, C, q, k, v, cos_t, sin_t, q_rot)
             elif only == "attn":
                 s["cache"].unstep_window_attn(f0, C, W, q_rot, out=out, workspace=ws)
-            elif events is None and not self.qknorm:
+            elif not self.qknorm:
                 s["cache"].unstep_step(f0, C, W, q, k, v, cos_t, sin_t, q_rot=q_rot, out=out, workspace=ws)
-            elif events is None:
-                self._append(s, f0, C, q, k, v, cos_t, sin_t, q_rot)
-                s["cache"].unstep_window_attn(f0, C, W, q_rot, out=out, workspace=ws)
             else:
-                e0, e1, e2 = (torch.cuda.Event(enable_timing=True) for _ in range(3))
-                e0.record()
                 self._append(s, f0, C, q, k, v, cos_t, sin_t, q_rot)
-                e1.record()
                 s["cache"].unstep_window_attn(f0, C, W, q_rot, out=out, workspace=ws)
-                e2.record()
-                events.append((e0, e1, e2, C * wl.T, self.keys(f0, C, W)))
         self.step_idx += 1
 
 
@@ -760,17 +829,10 @@ def measure_workload(u, torch, wl, n_sets, steps, warmup, qknorm=False):
     # calls, same rotating buffer sets) between two HIP events on the stream it runs on
     extra = {}
     if wl.name == "rolling":
-        # a stream's attention depends on the ring state its appends left: time the two
-        # kernels of each call between events around each of them instead
-        events = []
-        for _ in range(steps):
-            plan.step(events)
-        torch.cuda.synchronize()
-        app_ms = sum(e0.elapsed_time(e1) for (e0, e1, e2, _, _) in events) / steps
-        att_ms = sum(e1.elapsed_time(e2) for (e0, e1, e2, _, _) in events) / steps
+        app_ms, att = plan.time_rolling(steps)
         nc = len(plan.calls)
-        per_chunk = [sum(events[s * nc + c][1].elapsed_time(events[s * nc + c][2]) for s in range(steps)) * 1e3 / steps
-                     for c in range(nc)]
+        att_ms = sum(att) / steps
+        per_chunk = [sum(att[s * nc + c] for s in range(steps)) * 1e3 / steps for c in range(nc)]
         extra["attn_per_chunk_us"] = {"mean": round(sum(per_chunk) / nc, 2), "max": round(max(per_chunk), 2),
                                       "min": round(min(per_chunk), 2),
                                       "steady_12_frames_mean": round(sum(per_chunk[11:]) / len(per_chunk[11:]), 2)}
@@ -785,6 +847,13 @@ def measure_workload(u, torch, wl, n_sets, steps, warmup, qknorm=False):
     rope_gbs = per_call_bytes / (app_ms * 1e-3) / 1e9
     if ncalls > 1:
         extra["attn_us_per_step"] = round(att_ms * 1e3, 1)
+    # the bandwidth reference: q, k, v copied into three buffers in one launch per call
+    copy_ms = plan.time_copy_baseline(steps)
+    copy_bytes = sum(6 * 2 * wl.B * C * wl.T * wl.H * 128 for (_, f0, C, W) in plan.calls)
+    copy_gbs = copy_bytes / (copy_ms * 1e-3) / 1e9
+    extra["append_copy_baseline"] = {"kernel": "copy3", "us_per_call": round(copy_ms * 1e3 / ncalls, 2),
+                                     "bytes_per_call": copy_bytes // ncalls, "gbs": round(copy_gbs, 1),
+                                     "frac": round(copy_gbs / PEAK_HBM_GBS, 4)}
     app_kernel = "rope_norm_append_kernel" if qknorm else "rope_append_kernel"
     rec = {
         "value": round(flops / (ms * 1e-3) / 1e12, 3),
@@ -870,7 +939,7 @@ def main():
                           "frac": m["rope_append"]["frac"],
                           "traffic": measured_traffic(app_kernel, wl.name)},
     }
-    for k in ("attn_per_chunk_us", "attn_us_per_step"):
+    for k in ("attn_per_chunk_us", "attn_us_per_step", "append_copy_baseline"):
         if k in m:
             res[k] = m[k]
     # every other workload of the benchmark, measured in the same run (same box, same clock

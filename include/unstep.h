@@ -315,17 +315,25 @@ int unstep_svd_truncate(const float* w, int32_t rows, int32_t cols, int32_t rank
 
 /* y = x W^T + b: x bf16 [M, K] (e.g. the attention output [tokens, heads * 128]), w bf16
  * [N, K] (the nn.Linear layout [out, in]), bias bf16 [N] or NULL, y bf16 [M, N]; all
- * row-major and contiguous, on the device.  float32 accumulation and bias add, bf16 result
- * (a plain GEMM with a bias epilogue, run by hipBLASLt on hip_stream).  The first call on a
- * device creates the GEMM library's handle, and the first call on each (device, stream) a
- * 32 MB device workspace of its own, so calls on different streams may overlap (both kept
- * until the process ends); the first call for a shape times the library's candidate
- * algorithms on its own operands, synchronising the stream once, and keeps the fastest.
- * Calls from several host threads are serialised inside the library.
- * Errors: E_NULL (x, w, y), E_SHAPE (sizes < 1, K or N not a multiple of 8, no algorithm for
- * the shape), E_ALIGN, E_HIP. */
+ * row-major and contiguous, on the device.  float32 accumulation and bias add, one rounding to
+ * bf16 (nearest even).  One launch of the library's MFMA kernel on hip_stream: no scratch, no
+ * allocation, no synchronisation.  Errors: E_NULL (x, w, y), E_SHAPE (sizes < 1, K or N not a
+ * multiple of 8, more than 2^31 128 x 128 output tiles), E_ALIGN, E_HIP. */
 int unstep_linear(const void* x, const void* w, const void* bias, void* y, int32_t M, int32_t N, int32_t K,
                   void* hip_stream);
+
+/* ---------------------------------------------------------------------------------
+ * Measurement reference (not part of the method).
+ * ------------------------------------------------------------------------------- */
+
+/* x = a, y = b, z = c for three device buffers of `bytes` bytes each, in one launch with the
+ * access pattern of the fused RoPE + append pass (one thread per 16 bytes of each buffer,
+ * non-temporal stores): what a plain copy of that pass's bytes reaches, for comparing the
+ * pass's bandwidth against.  bytes must be a multiple of 16; pointers 16-byte aligned; the
+ * outputs must not overlap the inputs.  Errors: E_NULL, E_SHAPE (bytes < 0 or not a multiple
+ * of 16), E_ALIGN, E_HIP. */
+int unstep_copy3(const void* a, const void* b, const void* c, void* x, void* y, void* z, int64_t bytes,
+                 void* hip_stream);
 
 #ifdef __cplusplus
 }

@@ -60,6 +60,7 @@ SIGNATURES = {
     "unstep_linear": (ctypes.c_int, [_vp, _vp, _vp, _vp, _i32, _i32, _i32, _vp]),
     "unstep_sampler_calls": (ctypes.c_int, [_i32, _i32, _i32, _f64, _i32, _pi32, _pi32, _pi32, _pi32,
                                             ctypes.POINTER(_f64), ctypes.POINTER(_f64)]),
+    "unstep_copy3": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _vp]),
     "unstep_renoise": (ctypes.c_int, [_vp, _vp, _f64, _vp, _i64, _vp]),
     "unstep_emit": (ctypes.c_int, [_vp, _vp, _f64, _vp, _i64, _vp]),
     "unstep_window_attn": (ctypes.c_int, [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _f32, _vp, _sz, _vp]),
@@ -478,3 +479,15 @@ def unstep_emit(x_tilde: torch.Tensor, v: torch.Tensor, sigma: float, out: Optio
     _check(lib.unstep_emit(x_tilde.data_ptr(), v.data_ptr(), sigma, out.data_ptr(), x_tilde.numel(), _stream(stream)))
     _used_on(stream, out)
     return out
+
+
+def unstep_copy3(a: torch.Tensor, b: torch.Tensor, c: torch.Tensor, x: torch.Tensor, y: torch.Tensor,
+                 z: torch.Tensor, stream=None) -> None:
+    """x = a, y = b, z = c in one launch with the append pass's access pattern (a bandwidth
+    reference for that pass, not part of the method)."""
+    n = a.numel() * a.element_size()
+    for t in (a, b, c, x, y, z):
+        if not t.is_contiguous() or t.numel() * t.element_size() != n or t.device != a.device:
+            raise ValueError("six contiguous buffers of one size on one device")
+    _check(lib.unstep_copy3(a.data_ptr(), b.data_ptr(), c.data_ptr(), x.data_ptr(), y.data_ptr(), z.data_ptr(), n,
+                            _stream(stream)))

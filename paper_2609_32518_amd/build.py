@@ -5,8 +5,8 @@
 Run by path (not with -m): importing the package loads the library this script builds.
 
 Every source under csrc/ is compiled by hipcc to an object under _build/ and the
-objects are linked into paper_2609_32518_amd/libunstep.so, with ROCm's hipBLASLt (the
-projection GEMM), rocSOLVER and rocBLAS (the init-time SVD).  Device code is built
+objects are linked into paper_2609_32518_amd/libunstep.so, with ROCm's rocSOLVER and
+rocBLAS (the init-time SVD).  Device code is built
 with packed-fp32 instructions disabled.
 """
 from __future__ import annotations
@@ -66,7 +66,7 @@ def build(verbose: bool = False) -> str:
         objs = list(ex.map(lambda s: _compile(s, verbose), srcs))
     tmp = LIB + ".tmp"
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + objs + [
-        f"-L{ROCM}/lib", "-lhipblaslt", "-lrocsolver", "-lrocblas", f"-Wl,-rpath,{ROCM}/lib"]
+        f"-L{ROCM}/lib", "-lrocsolver", "-lrocblas", f"-Wl,-rpath,{ROCM}/lib"]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

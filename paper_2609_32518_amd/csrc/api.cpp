@@ -471,6 +471,19 @@ int flow_update(const char* where, const void* x, const void* y, void* out, int6
 }
 }  // namespace
 
+int unstep_copy3(const void* a, const void* b, const void* c, void* x, void* y, void* z, int64_t bytes,
+                 void* hip_stream) {
+  return unstep::guarded("unstep_copy3", [&]() -> int {
+    if (!a || !b || !c || !x || !y || !z) return fail(UNSTEP_E_NULL, "unstep_copy3: NULL buffer");
+    if (bytes < 0 || bytes % 16) return fail(UNSTEP_E_SHAPE, "unstep_copy3: bytes must be a multiple of 16");
+    if (!aligned16(a) || !aligned16(b) || !aligned16(c) || !aligned16(x) || !aligned16(y) || !aligned16(z))
+      return fail(UNSTEP_E_ALIGN, "unstep_copy3: pointers must be 16-byte aligned");
+    hipError_t e = unstep::launch_copy3(a, b, c, x, y, z, bytes / 16, static_cast<hipStream_t>(hip_stream));
+    if (e != hipSuccess) return fail(UNSTEP_E_HIP, "unstep_copy3: %s", hipGetErrorString(e));
+    return ok();
+  });
+}
+
 int unstep_renoise(const void* x, const void* eps, double sigma, void* x_tilde, int64_t n, void* hip_stream) {
   return unstep::guarded("unstep_renoise", [&]() -> int {
     return flow_update("unstep_renoise", x, eps, x_tilde, n, sigma, 1.0 - sigma, sigma, hip_stream);

@@ -77,6 +77,16 @@ struct AttnPlan {
 hipError_t launch_flow_update(const uint16_t* x, const uint16_t* y, uint16_t* out, int64_t n, double a, double b,
                               hipStream_t stream);
 
+// x = a, y = b, z = c on n16 pieces of 16 bytes each, one launch (the bandwidth reference of
+// the append pass); all pointers 16-byte aligned.
+hipError_t launch_copy3(const void* a, const void* b, const void* c, void* x, void* y, void* z, int64_t n16,
+                        hipStream_t stream);
+
+// y = x W^T + b: x bf16 [M, K], W bf16 [N, K], bias bf16 [N] or null, y bf16 [M, N], all
+// contiguous; K and N multiples of 8.
+hipError_t launch_linear(const uint16_t* x, const uint16_t* w, const uint16_t* bias, uint16_t* y, int32_t M,
+                         int32_t N, int32_t K, hipStream_t stream);
+
 // y = bf16(x) on n values, round to nearest even; x and y 16-byte aligned.
 hipError_t launch_cast_bf16(const float* x, uint16_t* y, int64_t n, hipStream_t stream);
 // y = double(x), and y = float(x) rounded to nearest even, on n values.

@@ -13,15 +13,9 @@
 // rounded to float32 and, optionally, to bf16 (the paper's cast).
 // Init-time only: it allocates scratch and synchronises the stream.
 //
-// unstep_linear: y = x W^T + b in bf16 with float32 accumulation, a plain GEMM with a bias
-// epilogue, run by hipBLASLt.  In column-major terms y^T [N, M] = W [N, K] x^T [K, M]: A = W
-// stored K x N (ld K) with op T, B = x stored K x M (ld K), D = y stored N x M (ld N); the bias
-// runs along D's rows.  Plans (descriptors + chosen algorithm) are cached per device and shape:
-// the first call on a device creates the library handle, the first call on a (device, stream)
-// a 32 MB workspace of its own, and the first call for a shape times hipBLASLt's candidate
-// algorithms on its own operands (synchronising once) and keeps the fastest.
+// unstep_linear: y = x W^T + b in bf16 with float32 accumulation, run by the hand-written MFMA
+// kernel of linear.hip (one launch, no scratch, no synchronisation).
 #include <hip/hip_runtime.h>
-#include <hipblaslt/hipblaslt.h>
 #include <rocblas/rocblas.h>
 #include <rocsolver/rocsolver.h>
 
@@ -57,129 +51,6 @@ rocblas_handle blas_handle(int dev) {
   if (rocblas_create_handle(&h) != rocblas_status_success) return nullptr;
   handles[dev] = h;
   return h;
-}
-
-// ---- hipBLASLt plans
-struct LinearPlan {
-  hipblasLtMatmulDesc_t desc = nullptr;
-  hipblasLtMatrixLayout_t a = nullptr, b = nullptr, d = nullptr;
-  hipblasLtMatmulAlgo_t algo{};
-};
-
-hipblasLtHandle_t lt_handle(int dev) {
-  static std::map<int, hipblasLtHandle_t> handles;
-  auto it = handles.find(dev);
-  if (it != handles.end()) return it->second;
-  hipblasLtHandle_t h = nullptr;
-  if (hipblasLtCreate(&h) != HIPBLAS_STATUS_SUCCESS) return nullptr;
-  handles[dev] = h;
-  return h;
-}
-
-constexpr size_t kLinearWorkspace = size_t(32) << 20;   // per device, for algorithms that want it
-constexpr int kCandidates = 64;
-
-// Device scratch of the GEMM library, one per (device, stream), allocated on the first call
-// that uses the pair: GEMMs enqueued on different streams may run at the same time, so they
-// must not share scratch; calls on one stream run in order and do.
-void* lt_workspace(int dev, hipStream_t st) {
-  static std::map<std::pair<int, hipStream_t>, void*> ws;
-  const auto key = std::make_pair(dev, st);
-  auto it = ws.find(key);
-  if (it != ws.end()) return it->second;
-  void* p = nullptr;
-  if (hipMalloc(&p, kLinearWorkspace) != hipSuccess) return nullptr;
-  ws[key] = p;
-  return p;
-}
-
-// Called with g_mu held.  The first call for a (device, shape) asks hipBLASLt for up to
-// kCandidates algorithms, times each on this call's operands (a few runs between events on the
-// call's stream, which synchronises once) and keeps the fastest.  Returns nullptr and sets *rc
-// (and the message) when the handle cannot be created or no algorithm fits the shape.
-const LinearPlan* linear_plan(int dev, int32_t M, int32_t N, int32_t K, const void* x, const void* w,
-                              const void* bias, void* y, hipStream_t st, hipblasLtHandle_t* h_out, void** ws_out,
-                              int* rc) {
-  static std::map<std::tuple<int, int32_t, int32_t, int32_t, bool>, LinearPlan> plans;
-  hipblasLtHandle_t h = lt_handle(dev);
-  void* ws = lt_workspace(dev, st);
-  *h_out = h;
-  *ws_out = ws;
-  if (!h || !ws) {
-    *rc = fail(UNSTEP_E_HIP, "unstep_linear: creating the GEMM handle or its workspace failed");
-    return nullptr;
-  }
-  const auto key = std::make_tuple(dev, M, N, K, bias != nullptr);
-  auto it = plans.find(key);
-  if (it != plans.end()) return &it->second;
-  LinearPlan p;
-  bool good = hipblasLtMatmulDescCreate(&p.desc, HIPBLAS_COMPUTE_32F, HIP_R_32F) == HIPBLAS_STATUS_SUCCESS;
-  const hipblasOperation_t ta = HIPBLAS_OP_T, tb = HIPBLAS_OP_N;
-  good = good && hipblasLtMatmulDescSetAttribute(p.desc, HIPBLASLT_MATMUL_DESC_TRANSA, &ta, sizeof ta) ==
-                     HIPBLAS_STATUS_SUCCESS;
-  good = good && hipblasLtMatmulDescSetAttribute(p.desc, HIPBLASLT_MATMUL_DESC_TRANSB, &tb, sizeof tb) ==
-                     HIPBLAS_STATUS_SUCCESS;
-  if (bias) {
-    const hipblasLtEpilogue_t ep = HIPBLASLT_EPILOGUE_BIAS;
-    const hipDataType bt = HIP_R_16BF;
-    good = good && hipblasLtMatmulDescSetAttribute(p.desc, HIPBLASLT_MATMUL_DESC_EPILOGUE, &ep, sizeof ep) ==
-                       HIPBLAS_STATUS_SUCCESS;
-    good = good && hipblasLtMatmulDescSetAttribute(p.desc, HIPBLASLT_MATMUL_DESC_BIAS_DATA_TYPE, &bt, sizeof bt) ==
-                       HIPBLAS_STATUS_SUCCESS;
-    good = good && hipblasLtMatmulDescSetAttribute(p.desc, HIPBLASLT_MATMUL_DESC_BIAS_POINTER, &bias, sizeof bias) ==
-                       HIPBLAS_STATUS_SUCCESS;
-  }
-  good = good && hipblasLtMatrixLayoutCreate(&p.a, HIP_R_16BF, K, N, K) == HIPBLAS_STATUS_SUCCESS;
-  good = good && hipblasLtMatrixLayoutCreate(&p.b, HIP_R_16BF, K, M, K) == HIPBLAS_STATUS_SUCCESS;
-  good = good && hipblasLtMatrixLayoutCreate(&p.d, HIP_R_16BF, N, M, N) == HIPBLAS_STATUS_SUCCESS;
-  hipblasLtMatmulPreference_t pref = nullptr;
-  good = good && hipblasLtMatmulPreferenceCreate(&pref) == HIPBLAS_STATUS_SUCCESS;
-  const uint64_t max_ws = kLinearWorkspace;
-  good = good && hipblasLtMatmulPreferenceSetAttribute(pref, HIPBLASLT_MATMUL_PREF_MAX_WORKSPACE_BYTES, &max_ws,
-                                                        sizeof max_ws) == HIPBLAS_STATUS_SUCCESS;
-  hipblasLtMatmulHeuristicResult_t res[kCandidates];
-  int found = 0;
-  good = good && hipblasLtMatmulAlgoGetHeuristic(h, p.desc, p.a, p.b, p.d, p.d, pref, kCandidates, res, &found) ==
-                     HIPBLAS_STATUS_SUCCESS;
-  if (pref) hipblasLtMatmulPreferenceDestroy(pref);
-  // time the candidates on this call's operands
-  int best = -1;
-  float best_ms = 0.f;
-  hipEvent_t e0 = nullptr, e1 = nullptr;
-  if (good && found > 1 && hipEventCreate(&e0) == hipSuccess && hipEventCreate(&e1) == hipSuccess) {
-    const float alpha = 1.f, beta = 0.f;
-    for (int i = 0; i < found; ++i) {
-      if (res[i].state != HIPBLAS_STATUS_SUCCESS || res[i].workspaceSize > kLinearWorkspace) continue;
-      bool ran = true;
-      for (int rep = 0; rep < 8 && ran; ++rep) {
-        if (rep == 3) (void)hipEventRecord(e0, st);
-        ran = hipblasLtMatmul(h, p.desc, &alpha, w, p.a, x, p.b, &beta, y, p.d, y, p.d, &res[i].algo, ws,
-                              kLinearWorkspace, st) == HIPBLAS_STATUS_SUCCESS;
-      }
-      float ms = 0.f;
-      if (!ran || hipEventRecord(e1, st) != hipSuccess || hipEventSynchronize(e1) != hipSuccess ||
-          hipEventElapsedTime(&ms, e0, e1) != hipSuccess)
-        continue;
-      if (best < 0 || ms < best_ms) {
-        best = i;
-        best_ms = ms;
-      }
-    }
-  } else if (good && found == 1) {
-    best = 0;
-  }
-  if (e0) (void)hipEventDestroy(e0);
-  if (e1) (void)hipEventDestroy(e1);
-  if (!good || best < 0) {
-    if (p.a) hipblasLtMatrixLayoutDestroy(p.a);
-    if (p.b) hipblasLtMatrixLayoutDestroy(p.b);
-    if (p.d) hipblasLtMatrixLayoutDestroy(p.d);
-    if (p.desc) hipblasLtMatmulDescDestroy(p.desc);
-    *rc = fail(UNSTEP_E_SHAPE, "unstep_linear: no hipBLASLt algorithm for M=%d N=%d K=%d", M, N, K);
-    return nullptr;
-  }
-  p.algo = res[best].algo;
-  return &(plans[key] = p);
 }
 
 template <typename T>
@@ -278,26 +149,14 @@ int unstep_linear(const void* x, const void* w, const void* bias, void* y, int32
     if (!x || !w || !y) return fail(UNSTEP_E_NULL, "%s: x, w and y are required", where);
     if (M < 1 || N < 1 || K < 1) return fail(UNSTEP_E_SHAPE, "%s: M, N, K must be >= 1", where);
     if (K % 8 || N % 8) return fail(UNSTEP_E_SHAPE, "%s: K and N must be multiples of 8", where);
+    if ((int64_t(M) + 127) / 128 * ((int64_t(N) + 127) / 128) > INT32_MAX)
+      return fail(UNSTEP_E_SHAPE, "%s: too many 128 x 128 output tiles for one launch", where);
     if (!aligned16(x) || !aligned16(w) || !aligned16(y) || (bias && !aligned16(bias)))
       return fail(UNSTEP_E_ALIGN, "%s: pointers must be 16-byte aligned", where);
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
+    hipError_t e = unstep::launch_linear(static_cast<const uint16_t*>(x), static_cast<const uint16_t*>(w),
+                                         static_cast<const uint16_t*>(bias), static_cast<uint16_t*>(y), M, N, K,
+                                         static_cast<hipStream_t>(hip_stream));
     if (e != hipSuccess) return hip_fail(where, e);
-    // the plan's descriptor carries the bias pointer: set it and enqueue under the lock
-    std::lock_guard<std::mutex> lk(g_mu);
-    hipStream_t st = static_cast<hipStream_t>(hip_stream);
-    hipblasLtHandle_t h = nullptr;
-    void* ws = nullptr;
-    int rc = UNSTEP_OK;
-    const LinearPlan* p = linear_plan(dev, M, N, K, x, w, bias, y, st, &h, &ws, &rc);
-    if (!p) return rc;
-    if (bias && hipblasLtMatmulDescSetAttribute(p->desc, HIPBLASLT_MATMUL_DESC_BIAS_POINTER, &bias, sizeof bias) !=
-                    HIPBLAS_STATUS_SUCCESS)
-      return fail(UNSTEP_E_HIP, "%s: setting the bias pointer failed", where);
-    const float alpha = 1.f, beta = 0.f;
-    if (hipblasLtMatmul(h, p->desc, &alpha, w, p->a, x, p->b, &beta, y, p->d, y, p->d, &p->algo, ws, kLinearWorkspace,
-                        st) != HIPBLAS_STATUS_SUCCESS)
-      return fail(UNSTEP_E_HIP, "%s: hipblasLtMatmul failed", where);
     return ok();
   });
 }

@@ -486,3 +486,14 @@ def test_noalloc_attention_checks_arguments_before_any_device_work():
         assert f(h, 5, 3, 0, FAKE[2], FAKE[3], None, 0.0, None) == u.E_STATE
     finally:
         u.lib.unstep_cache_destroy(h)
+
+
+def test_copy_reference_argument_errors():
+    f = u.lib.unstep_copy3
+    p = FAKE
+    assert f(None, p[1], p[2], p[3], p[4], p[5], 64, None) == u.E_NULL
+    assert f(p[0], p[1], p[2], p[3], p[4], None, 64, None) == u.E_NULL
+    assert f(p[0], p[1], p[2], p[3], p[4], p[5], 60, None) == u.E_SHAPE
+    assert f(p[0], p[1], p[2], p[3], p[4], p[5], -16, None) == u.E_SHAPE
+    assert f(p[0] + 8, p[1], p[2], p[3], p[4], p[5], 64, None) == u.E_ALIGN
+    assert f(p[0], p[1], p[2], p[3], p[4], p[5], 0, None) == u.OK          # nothing to copy, nothing launched

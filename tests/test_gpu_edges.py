@@ -195,3 +195,14 @@ def test_snapshot_restore_through_advance():
         want, _ = m.expected(rope.rope_bf16(q, c, s), 15 + 3 * n, 3, 3)
         check_attention(host(outs[1]), want, f"restored cache call {n}")
     m.check_cache("after the restored run")
+
+
+def test_copy_reference_copies_bits():
+    # the append pass's bandwidth reference: three buffers copied bit for bit, a ragged piece count
+    n = 3 * 257 * 8 + 8                                   # 16-byte pieces, not a multiple of 256 threads
+    src = [torch.randint(-32768, 32767, (n,), dtype=torch.int16, device="cuda") for _ in range(3)]
+    dst = [torch.zeros_like(t) for t in src]
+    u.unstep_copy3(*src, *dst)
+    torch.cuda.synchronize()
+    for a, b in zip(src, dst):
+        assert torch.equal(a, b)
