@@ -58,6 +58,9 @@ def parse():
     p.add_argument("--sub-steps", type=int, default=10, help="timed steps of each other workload's record")
     p.add_argument("--sub-warmup", type=int, default=10)
     p.add_argument("--sets", type=int, default=6)
+    p.add_argument("--no-split", action="store_true",
+                   help="attention without a workspace: one work-group per query tile over its whole key "
+                        "range, whatever the plan would pick")
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--qknorm", action="store_true",
                    help="append with the fused RMS normalisation of q and k (unstep_kv_append_qknorm), "
@@ -111,7 +114,7 @@ def rope_bytes(H, Nq, D=128):
 class Plan:
     """The step's work for one workload: a list of (cache set, start frame, frames, window)."""
 
-    def __init__(self, u, torch, wl, n_sets, qknorm=False):
+    def __init__(self, u, torch, wl, n_sets, qknorm=False, no_split=False):
         self.u, self.torch, self.wl = u, torch, wl
         dev = "cuda"
         g = torch.Generator(device=dev)
@@ -122,6 +125,7 @@ class Plan:
             return torch.randn(shape, generator=g, device=dev, dtype=torch.float32).to(torch.bfloat16)
 
         self.qknorm = qknorm
+        self.no_split = no_split
         if qknorm:
             # learned-norm-like weights around 1
             g.manual_seed(7)
@@ -155,7 +159,7 @@ class Plan:
         for (_, f0, C, W) in self.calls:
             self.tables.get(f0, C, wl.grid_h, wl.grid_w)
         self.ws = {}
-        for si, s in enumerate(self.sets):
+        for si, s in enumerate(self.sets if not no_split else []):
             for (_, f0, C, W) in self.calls:
                 need = s["cache"].workspace_bytes(f0, C, W)
                 if need and need > self.ws.get(si, torch.empty(0)).numel():
@@ -257,7 +261,8 @@ class Plan:
                     a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
                     a.record()
                     cache.unstep_window_attn(f0, C, W, s["q_rot"][:, :N], out=s["out"][:, :N],
-                                             workspace=self.ws.get(self.step_idx % len(self.sets)))
+                                             workspace=self.ws.get(self.step_idx % len(self.sets)),
+                                             use_split=not self.no_split)
                     b.record()
                     att.append((a, b))
             self.step_idx += 1
@@ -307,12 +312,13 @@ class Plan:
             if only == "append":
                 self._append(s, f0, C, q, k, v, cos_t, sin_t, q_rot)
             elif only == "attn":
-                s["cache"].unstep_window_attn(f0, C, W, q_rot, out=out, workspace=ws)
+                s["cache"].unstep_window_attn(f0, C, W, q_rot, out=out, workspace=ws, use_split=not self.no_split)
             elif not self.qknorm:
-                s["cache"].unstep_step(f0, C, W, q, k, v, cos_t, sin_t, q_rot=q_rot, out=out, workspace=ws)
+                s["cache"].unstep_step(f0, C, W, q, k, v, cos_t, sin_t, q_rot=q_rot, out=out, workspace=ws,
+                                       use_split=not self.no_split)
             else:
                 self._append(s, f0, C, q, k, v, cos_t, sin_t, q_rot)
-                s["cache"].unstep_window_attn(f0, C, W, q_rot, out=out, workspace=ws)
+                s["cache"].unstep_window_attn(f0, C, W, q_rot, out=out, workspace=ws, use_split=not self.no_split)
         self.step_idx += 1
 
 
@@ -807,11 +813,11 @@ def clip_bench(u, torch, args):
 SUB_WORKLOADS = ("tiny", "unwindowed", "short_refine", "rolling", "paper_default")
 
 
-def measure_workload(u, torch, wl, n_sets, steps, warmup, qknorm=False):
+def measure_workload(u, torch, wl, n_sets, steps, warmup, qknorm=False, no_split=False):
     """Time `steps` whole steps of a workload after `warmup` untimed ones, then each kernel of the
     step on its own; returns the figures of one bench record (attention and append per call,
     with their roofline fractions, and the step)."""
-    plan = Plan(u, torch, wl, n_sets, qknorm=qknorm)
+    plan = Plan(u, torch, wl, n_sets, qknorm=qknorm, no_split=no_split)
     flops, _ = plan.per_step()
     torch.cuda.synchronize()
     for _ in range(warmup):
@@ -921,7 +927,8 @@ def main():
         return
     headline = args.workload or "full_chunk"
     wl = synth.WORKLOADS[headline]
-    m = measure_workload(u, torch, wl, args.sets, args.steps, args.warmup, qknorm=args.qknorm)
+    m = measure_workload(u, torch, wl, args.sets, args.steps, args.warmup, qknorm=args.qknorm,
+                         no_split=args.no_split)
     app_kernel = "rope_norm_append_kernel" if args.qknorm else "rope_append_kernel"
     res = {
         "metric": METRIC, "value": m["value"], "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
