@@ -201,30 +201,37 @@ class Plan:
             return call_set
         return self.step_idx % len(self.sets)
 
-    def behind_wait(self, enqueue, steps, spin=True):
-        """Run enqueue() `steps` times between two HIP events on the current stream after one
-        untimed pass (which also loads the kernels).  spin: enqueue it all behind a device-side
-        spin long enough for the host to enqueue every launch first, so that the events bracket
-        GPU time only, with no host enqueue gap; for kernels short against the binding's host
-        time.  Kernels much longer than it (attention) run without the spin: a spin leaves the
-        power-limited chip in a different clock state than the step loop does.  Returns ms per
-        pass."""
+    def behind_wait(self, enqueue, steps, spin=True, launches_per_pass=1):
+        """Run enqueue() `steps` times between HIP events on the current stream after one untimed
+        pass (which also loads the kernels).  spin: for kernels short against the binding's host
+        time, enqueue the passes in batches of at most ~128 launches, each batch behind a
+        device-side spin long enough for the host to enqueue the whole batch first (a batch fits
+        the hardware queue), so that the events bracket GPU time only, with no host enqueue gap.
+        Kernels much longer than the host time (attention) run without the spin: a spin leaves
+        the power-limited chip in a different clock state than the step loop does.  Returns ms
+        per pass."""
         torch = self.torch
         torch.cuda.synchronize()
         t0 = time.perf_counter()
         enqueue()                                    # untimed pass: loads the kernels, sizes the wait
         t_host = time.perf_counter() - t0
-        if spin:
-            torch.cuda.synchronize()
-            wait_s = min(1.0, 2.0 * t_host * steps + 2e-3)
-            torch.cuda._sleep(int(wait_s * 2.5e9))  # spin counted in shader cycles (<= 2.4 GHz)
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(steps):
-            enqueue()
-        e1.record()
         torch.cuda.synchronize()
-        return e0.elapsed_time(e1) / steps
+        batch = max(1, 128 // max(1, launches_per_pass)) if spin else steps
+        total_ms, done = 0.0, 0
+        while done < steps:
+            n = min(batch, steps - done)
+            if spin:
+                wait_s = min(1.0, 2.0 * t_host * n + 2e-3)
+                torch.cuda._sleep(int(wait_s * 2.5e9))   # spin counted in shader cycles (<= 2.4 GHz)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(n):
+                enqueue()
+            e1.record()
+            torch.cuda.synchronize()
+            total_ms += e0.elapsed_time(e1)
+            done += n
+        return total_ms / steps
 
     def time_kernels(self, steps):
         """Average per-step time (ms) of the appends and of the attention calls, each launched
@@ -232,7 +239,8 @@ class Plan:
         out = []
         for which in ("append", "attn"):
             self.step_idx = 0
-            out.append(self.behind_wait(lambda: self.step(only=which), steps, spin=which == "append"))
+            out.append(self.behind_wait(lambda: self.step(only=which), steps, spin=which == "append",
+                                        launches_per_pass=len(self.calls)))
         return out
 
     def time_rolling(self, steps):
@@ -268,7 +276,7 @@ class Plan:
             self.step_idx += 1
 
         self.step_idx = 0
-        app_ms = self.behind_wait(lambda: one_step("append"), steps, spin=True)
+        app_ms = self.behind_wait(lambda: one_step("append"), steps, spin=True, launches_per_pass=len(self.calls))
         self.step_idx = 0
         self.behind_wait(lambda: one_step("attn"), steps, spin=False)
         return app_ms, [a.elapsed_time(b) for (a, b) in att[len(self.calls):]]    # the untimed pass dropped
@@ -291,7 +299,7 @@ class Plan:
             self.step_idx += 1
 
         self.step_idx = 0
-        return self.behind_wait(one_step, steps, spin=True)
+        return self.behind_wait(one_step, steps, spin=True, launches_per_pass=len(self.calls))
 
     def step(self, only=None):
         """Enqueue one step (only="append" / "attn": just that kernel of each call)."""
@@ -361,11 +369,12 @@ def cpu_baseline(wl, n_queries):
 
 
 
+_CSRC = "paper_2609_32518_amd/csrc/"
 KERNEL_SOURCES = {
-    "window_attn_kernel": ["paper_2609_32518_amd/csrc/window_attn.hip", "paper_2609_32518_amd/csrc/kernels.hpp"],
-    "rope_append_kernel": ["paper_2609_32518_amd/csrc/rope_append.hip", "paper_2609_32518_amd/csrc/kernels.hpp"],
-    "rope_norm_append_kernel": ["paper_2609_32518_amd/csrc/rope_append.hip",
-                                "paper_2609_32518_amd/csrc/kernels.hpp"],
+    "window_attn_kernel": [_CSRC + "window_attn.hip", _CSRC + "kernels.hpp", _CSRC + "seg_table.hpp"],
+    "rope_append_kernel": [_CSRC + "rope_append.hip", _CSRC + "kernels.hpp", _CSRC + "seg_table.hpp"],
+    "rope_norm_append_kernel": [_CSRC + "rope_append.hip", _CSRC + "kernels.hpp", _CSRC + "seg_table.hpp"],
+    "copy3_kernel": [_CSRC + "copy_baseline.hip", _CSRC + "kernels.hpp"],
 }
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 
@@ -457,8 +466,10 @@ def summarize_profile(d, workload="full_chunk", qknorm=False):
     # end of the run: the same dispatches' average, for comparison with its HIP-event figure
     trace_rows = sorted(csv.DictReader(open(os.path.join(d, "trace", "trace_kernel_trace.csv"))),
                         key=lambda r: int(r["Start_Timestamp"]))
-    steps = 30
-    for kern in ("window_attn_kernel", "rope_append_kernel<true>", "rope_norm_append_kernel<true, 3>"):
+    import synth
+    wl = synth.WORKLOADS[workload]
+    steps = 30 * wl.layers * wl.passes        # dispatches of the timing loop: 30 steps of the workload's calls
+    for kern in ("window_attn_kernel", "rope_append_kernel<true>", "rope_norm_append_kernel<true, 3>", "copy3_kernel"):
         durs = [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in trace_rows if kname(r["Kernel_Name"]) == kern]
         if workload == "rolling" and durs:
             # the stream's bench times every call between events: its figure is the average over
@@ -477,13 +488,13 @@ def summarize_profile(d, workload="full_chunk", qknorm=False):
         lines[-3:-2] = ["", "Per-dispatch figures here and below are averages over the stream's calls, whose "
                         "key ranges grow from 1 to 12 frames.", ""]
     for k in sorted(set(fetch) | set(write)):
-        if not k.startswith(("window_attn", "attn_combine", "rope_append", "rope_norm_append")):
+        if not k.startswith(("window_attn", "attn_combine", "rope_append", "rope_norm_append", "copy3")):
             continue
         fk, wk = fetch.get(k, {}).get("FETCH_SIZE", 0.0), write.get(k, {}).get("WRITE_SIZE", 0.0)
         rb, wb = fk * 1024 * f_scale, wk * 1024 * w_scale
         lines.append(f"| {k} | {fk:.0f} | {wk:.0f} | {rb / 1e6:.2f} | {wb / 1e6:.2f} | {(rb + wb) / 1e6:.2f} |")
         base = k.split("<")[0]
-        if base in KERNEL_SOURCES and (base == "window_attn_kernel" or k.startswith(base + "<true")):
+        if base in KERNEL_SOURCES and (base in ("window_attn_kernel", "copy3_kernel") or k.startswith(base + "<true")):
             traffic[workload][base] = {"bytes_per_launch": round(rb + wb), "read_bytes": round(rb),
                                        "write_bytes": round(wb), "source": source_hash(base)}
     a = sq.get("window_attn_kernel")
@@ -859,7 +870,8 @@ def measure_workload(u, torch, wl, n_sets, steps, warmup, qknorm=False, no_split
     copy_gbs = copy_bytes / (copy_ms * 1e-3) / 1e9
     extra["append_copy_baseline"] = {"kernel": "copy3", "us_per_call": round(copy_ms * 1e3 / ncalls, 2),
                                      "bytes_per_call": copy_bytes // ncalls, "gbs": round(copy_gbs, 1),
-                                     "frac": round(copy_gbs / PEAK_HBM_GBS, 4)}
+                                     "frac": round(copy_gbs / PEAK_HBM_GBS, 4),
+                                     "traffic": measured_traffic("copy3_kernel", wl.name)}
     app_kernel = "rope_norm_append_kernel" if qknorm else "rope_append_kernel"
     rec = {
         "value": round(flops / (ms * 1e-3) / 1e12, 3),
