@@ -102,6 +102,36 @@ def parse():
     return p.parse_args()
 
 
+def timed_passes(torch, enqueue, passes, spin=True, batch=128):
+    """Run enqueue() `passes` times between HIP events on the current stream after one untimed
+    pass (which also loads the kernels and sizes the wait); returns ms per pass.  spin: for
+    launches short against the binding's host time, enqueue the passes in batches of `batch`,
+    each behind a device-side spin long enough for the host to enqueue the whole batch first (a
+    batch fits the hardware queue), so that the events bracket GPU time only, with no host
+    enqueue gap between launches."""
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    enqueue()
+    t_host = time.perf_counter() - t0
+    torch.cuda.synchronize()
+    batch = batch if spin else passes
+    total_ms, done = 0.0, 0
+    while done < passes:
+        n = min(batch, passes - done)
+        if spin:
+            wait_s = min(1.0, 2.0 * t_host * n + 2e-3)
+            torch.cuda._sleep(int(wait_s * 2.5e9))   # spin counted in shader cycles (<= 2.4 GHz)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            enqueue()
+        e1.record()
+        torch.cuda.synchronize()
+        total_ms += e0.elapsed_time(e1)
+        done += n
+    return total_ms / passes
+
+
 def attn_flops(H, Nq, Nk, D=128):
     return 4.0 * H * Nq * Nk * D
 
@@ -202,36 +232,11 @@ class Plan:
         return self.step_idx % len(self.sets)
 
     def behind_wait(self, enqueue, steps, spin=True, launches_per_pass=1):
-        """Run enqueue() `steps` times between HIP events on the current stream after one untimed
-        pass (which also loads the kernels).  spin: for kernels short against the binding's host
-        time, enqueue the passes in batches of at most ~128 launches, each batch behind a
-        device-side spin long enough for the host to enqueue the whole batch first (a batch fits
-        the hardware queue), so that the events bracket GPU time only, with no host enqueue gap.
-        Kernels much longer than the host time (attention) run without the spin: a spin leaves
+        """timed_passes() on this plan's torch; spin only for kernels short against the host
+        time: kernels much longer than it (attention) run without the spin, since a spin leaves
         the power-limited chip in a different clock state than the step loop does.  Returns ms
         per pass."""
-        torch = self.torch
-        torch.cuda.synchronize()
-        t0 = time.perf_counter()
-        enqueue()                                    # untimed pass: loads the kernels, sizes the wait
-        t_host = time.perf_counter() - t0
-        torch.cuda.synchronize()
-        batch = max(1, 128 // max(1, launches_per_pass)) if spin else steps
-        total_ms, done = 0.0, 0
-        while done < steps:
-            n = min(batch, steps - done)
-            if spin:
-                wait_s = min(1.0, 2.0 * t_host * n + 2e-3)
-                torch.cuda._sleep(int(wait_s * 2.5e9))   # spin counted in shader cycles (<= 2.4 GHz)
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record()
-            for _ in range(n):
-                enqueue()
-            e1.record()
-            torch.cuda.synchronize()
-            total_ms += e0.elapsed_time(e1)
-            done += n
-        return total_ms / steps
+        return timed_passes(self.torch, enqueue, steps, spin, max(1, 128 // max(1, launches_per_pass)))
 
     def time_kernels(self, steps):
         """Average per-step time (ms) of the appends and of the attention calls, each launched
@@ -643,19 +648,23 @@ def oproj_bench(u, torch, args):
     y = torch.empty((M, N), dtype=torch.bfloat16, device=dev)
     for k in range(max(args.warmup, 20)):
         u.unstep_linear(xs[k % 16], w, b, out=y)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
     n = max(args.steps, 100)
-    e0.record()
-    for k in range(n):
-        u.unstep_linear(xs[k % 16], w, b, out=y)
-    e1.record()
-    torch.cuda.synchronize()
-    us = e0.elapsed_time(e1) * 1e3 / n
+    it = [0]
+
+    def call():
+        u.unstep_linear(xs[it[0] % 16], w, b, out=y)
+        it[0] += 1
+
+    # kernel time: behind the device-side spin (the binding's host time per call is comparable to
+    # the kernel's, so back-to-back calls alone would time the host); then the same calls without
+    # the spin, the rate a Python caller gets
+    us = timed_passes(torch, call, n, spin=True, batch=50) * 1e3
+    us_host = timed_passes(torch, call, n, spin=False) * 1e3
     flops = 2.0 * M * N * K
     tf = flops / (us * 1e-6) / 1e12
     print(json.dumps({"metric": "output projection µs per chunk (4680 x 1536 x 1536 bf16 + bias)",
                       "value": round(us, 2), "unit": "us", "higher_is_better": False, "calls": n,
+                      "us_per_call_back_to_back_through_binding": round(us_host, 2),
                       "tflops": round(tf, 1), "frac_of_bf16_peak": round(tf / PEAK_BF16_TFLOPS, 4),
                       "svd_truncate_ms": {"first_call": round(svd_ms, 1), "second_call": round(svd_ms2, 1),
                                           "shape": [N, K], "rank": r},
@@ -683,17 +692,20 @@ def flow_update_bench(u, torch, args):
 
     for k in range(args.warmup):
         run(k)
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    e0.record()
-    for k in range(args.steps):
-        run(k)
-    e1.record()
-    torch.cuda.synchronize()
-    us_pair = e0.elapsed_time(e1) * 1e3 / args.steps
+    it = [0]
+
+    def pair():
+        run(it[0])
+        it[0] += 1
+
+    # kernel time behind the device-side spin (a pair's host time through the binding is several
+    # times its GPU time), then the rate of back-to-back calls from Python
+    us_pair = timed_passes(torch, pair, args.steps, spin=True, batch=64) * 1e3
+    us_host = timed_passes(torch, pair, args.steps, spin=False) * 1e3
     nbytes = 2 * 3 * 2 * n                       # two ops, each reads two bf16 tensors and writes one
     print(json.dumps({"metric": "clean-cache renoise + emit µs per chunk latent", "value": round(us_pair, 3),
                       "unit": "us", "higher_is_better": False, "steps": args.steps, "warmup": args.warmup,
+                      "us_per_pair_back_to_back_through_binding": round(us_host, 3),
                       "bytes": nbytes, "gbs": round(nbytes / (us_pair * 1e-6) / 1e9, 1),
                       "hbm_frac": round(nbytes / (us_pair * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
                       "config": {"latent": list(shape), "sigma": sigma}, "dtype": "bf16 in/out, f64 math",

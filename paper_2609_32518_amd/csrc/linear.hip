@@ -180,7 +180,11 @@ __global__ __launch_bounds__(kThreads, 2) void linear_kernel(LinearArgs a) {
 // physical chunk l % 8, so it fetches logical chunk (l % 8) ^ swz(row).  Loaders issue stage
 // s + 2 while stage s is multiplied and wait for stage s + 1 before the barrier that ends the
 // step, which also frees stage s's ring slot; issuing a direct-to-LDS load stalls the issuing
-// wave, so keeping the loads off the multiplying waves keeps their MFMA stream going.
+// wave, so keeping the loads off the multiplying waves keeps their MFMA stream going.  After the
+// k loop the multiplying waves add the bias (loaded before the loop) and write the rounded tile
+// into the then free ring, and all 8 waves store it in 16-byte pieces that cover whole row runs
+// (each lane's own results are 8-byte pieces of 32 different rows, which stored directly made
+// every store instruction touch 32 partial cache lines).
 constexpr int kBigBM = 256;
 constexpr int kBigStages = 3;
 constexpr int kWBytes = kBN * kRowBytes;                  // 16 KB
@@ -224,46 +228,30 @@ __device__ __forceinline__ bf16x8_t frag(const uint32_t (&w_off)[4], const uint3
 }
 
 constexpr int kPCThreads = 512;
+// output staging after the k loop: the 256 x 128 bf16 tile in LDS rows of 272 bytes (16-byte
+// aligned; consecutive rows start 4 banks apart, so the multiplying waves' 8-byte writes of 32
+// rows at one column conflict at most 2-way)
+constexpr int kYPitch = 272;
+static_assert(kBigBM * kYPitch <= kBigStages * kStageBytes, "the y tile must fit the LDS ring");
 
-__global__ __launch_bounds__(kPCThreads, 1) void linear_kernel_big(LinearArgs a) {
-  __shared__ __attribute__((aligned(1024))) uint8_t lds[kBigStages * kStageBytes];
-
-  const int tid = threadIdx.x;
-  const int lane = tid & 63;
-  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const bool loader = wave >= 4;
-  const int lw = wave & 3;                     // loader index or multiplier index
+// The multiplying waves of linear_kernel_big: the k loop over the LDS ring, then the tile, bias
+// added in float32 and rounded once, written to LDS rows of kYPitch bytes.
+__device__ __forceinline__ void multiply(const LinearArgs& a, uint32_t lds0, int lw, int lane, int32_t n0,
+                                         int32_t m0, int32_t steps) {
   const int wn = lw >> 1, wm = lw & 1;
   const int col = lane & 31, half = lane >> 5;
 
-  const int32_t G = gridDim.x;
-  const int32_t xcd = blockIdx.x % kXcds;
-  const int32_t g = xcd * (G / kXcds) + min(xcd, G % kXcds) + blockIdx.x / kXcds;
-  const int32_t tn = g % a.tiles_n, tm = g / a.tiles_n;
-  const int32_t n0 = tn * kBN, m0 = tm * kBigBM;
-  const uint32_t lds0 = uint32_t(uintptr_t((__attribute__((address_space(3))) void*)lds));
-  const int32_t steps = a.K / kBK;
-
-  if (loader) {
+  // this lane's bias values, loaded before the loop so that their latency is hidden: columns
+  // n0 + wn*64 + nb*32 + 8 gq + 4 half + e (N is a multiple of 8: a run of 4 is all in or all out)
+  typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+  u32x2_t bq[2][4];
 #pragma unroll
-    for (int j = 0; j < kLoadsPerWave; ++j) big_load(a, lds0, lw, lane, j, n0, m0, 0);
-    if (steps > 1)
+  for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
-      for (int j = 0; j < kLoadsPerWave; ++j) big_load(a, lds0 + kStageBytes, lw, lane, j, n0, m0, kBK);
-    wait_loads(steps > 1);                     // stage 0
-    big_barrier();
-    for (int32_t s = 0; s < steps; ++s) {
-      const bool more = s + 2 < steps;
-      if (more) {
-        const uint32_t nxt = lds0 + uint32_t(((s + 2) % kBigStages) * kStageBytes);
-#pragma unroll
-        for (int j = 0; j < kLoadsPerWave; ++j) big_load(a, nxt, lw, lane, j, n0, m0, (s + 2) * kBK);
-      }
-      if (s + 1 < steps) wait_loads(more);     // stage s + 1 (stage s + 2 may still be in flight)
-      big_barrier();
+    for (int gq = 0; gq < 4; ++gq) {
+      const int32_t n = n0 + wn * 64 + nb * 32 + 8 * gq + 4 * half;
+      bq[nb][gq] = (a.bias && n < a.N) ? *reinterpret_cast<const u32x2_t*>(a.bias + n) : u32x2_t{0u, 0u};
     }
-    return;
-  }
 
   // fragment offsets within a stage: W row wn*64 + nb*32 + col, x row wm*128 + mb*32 + col, chunk
   // 2 kk + half; rows 32 apart share the swizzle (nb, mb are immediate offsets)
@@ -306,26 +294,80 @@ __global__ __launch_bounds__(kPCThreads, 1) void linear_kernel_big(LinearArgs a)
     big_barrier();                             // stage s read; stage s + 1 has landed
   }
 
+  // lane holds y[m][n .. n + 3] for tile row wm*128 + mb*32 + col and tile columns
+  // wn*64 + nb*32 + 8 gq + 4 half; rows past M or N hold finite values and are not stored
   typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
 #pragma unroll
   for (int mb = 0; mb < 4; ++mb) {
-    const int32_t m = m0 + wm * 128 + mb * 32 + col;
-    if (m >= a.M) continue;
+    const int r = wm * 128 + mb * 32 + col;
 #pragma unroll
     for (int nb = 0; nb < 2; ++nb)
 #pragma unroll
       for (int gq = 0; gq < 4; ++gq) {
-        const int32_t n = n0 + wn * 64 + nb * 32 + 8 * gq + 4 * half;
-        if (n >= a.N) continue;
-        bf16x4_t r;
+        const int cn = wn * 64 + nb * 32 + 8 * gq + 4 * half;
+        bf16x4_t v;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          float v = acc[nb][mb][4 * gq + e];
-          if (a.bias) v += __uint_as_float(uint32_t(a.bias[n + e]) << 16);
-          r[e] = (__bf16)v;
+          const uint32_t b2 = bq[nb][gq][e >> 1];
+          const float bias = __uint_as_float((e & 1) ? (b2 & 0xffff0000u) : (b2 << 16));
+          v[e] = (__bf16)(acc[nb][mb][4 * gq + e] + bias);
         }
-        *reinterpret_cast<bf16x4_t*>(a.y + int64_t(m) * a.N + n) = r;
+        *reinterpret_cast<__attribute__((address_space(3))) bf16x4_t*>(uintptr_t(lds0 + uint32_t(r * kYPitch + cn * 2))) = v;
       }
+  }
+}
+
+
+__global__ __launch_bounds__(kPCThreads, 1) void linear_kernel_big(LinearArgs a) {
+  __shared__ __attribute__((aligned(1024))) uint8_t lds[kBigStages * kStageBytes];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const bool loader = wave >= 4;
+  const int lw = wave & 3;                     // loader index or multiplier index
+
+  const int32_t G = gridDim.x;
+  const int32_t xcd = blockIdx.x % kXcds;
+  const int32_t g = xcd * (G / kXcds) + min(xcd, G % kXcds) + blockIdx.x / kXcds;
+  const int32_t tn = g % a.tiles_n, tm = g / a.tiles_n;
+  const int32_t n0 = tn * kBN, m0 = tm * kBigBM;
+  const uint32_t lds0 = uint32_t(uintptr_t((__attribute__((address_space(3))) void*)lds));
+  const int32_t steps = a.K / kBK;
+
+  if (loader) {
+#pragma unroll
+    for (int j = 0; j < kLoadsPerWave; ++j) big_load(a, lds0, lw, lane, j, n0, m0, 0);
+    if (steps > 1)
+#pragma unroll
+      for (int j = 0; j < kLoadsPerWave; ++j) big_load(a, lds0 + kStageBytes, lw, lane, j, n0, m0, kBK);
+    wait_loads(steps > 1);                     // stage 0
+    big_barrier();
+    for (int32_t s = 0; s < steps; ++s) {
+      const bool more = s + 2 < steps;
+      if (more) {
+        const uint32_t nxt = lds0 + uint32_t(((s + 2) % kBigStages) * kStageBytes);
+#pragma unroll
+        for (int j = 0; j < kLoadsPerWave; ++j) big_load(a, nxt, lw, lane, j, n0, m0, (s + 2) * kBK);
+      }
+      if (s + 1 < steps) wait_loads(more);     // stage s + 1 (stage s + 2 may still be in flight)
+      big_barrier();
+    }
+  } else {
+    multiply(a, lds0, lw, lane, n0, m0, steps);
+  }
+  big_barrier();                               // the y tile is in LDS (the ring is free)
+
+  // all 8 waves store the tile: thread t moves 16-byte piece t % 16 (columns n0 + 8 (t % 16) ..
+  // + 7) of tile rows t / 16 + 32 i, so that a wave writes four whole 256-byte row runs
+  const int c = tid & 15;
+  const int32_t n = n0 + 8 * c;
+#pragma unroll
+  for (int i = 0; i < kBigBM / 32; ++i) {
+    const int r = (tid >> 4) + 32 * i;
+    const int32_t m = m0 + r;
+    const u32x4_t v = *reinterpret_cast<const lds_u32x4_t*>(uintptr_t(lds0 + uint32_t(r * kYPitch + c * 16)));
+    if (m < a.M && n < a.N) *reinterpret_cast<u32x4_t*>(a.y + int64_t(m) * a.N + n) = v;
   }
 }
 
