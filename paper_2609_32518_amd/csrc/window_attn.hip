@@ -65,6 +65,10 @@ constexpr int kAhead = kStages - 1;           // stages in flight ahead of the o
 constexpr int kDmaPerStage = 4;               // direct-to-LDS loads per wave per stage
 constexpr int kRowBytes = kHeadDim * 2;       // one K or V row (bf16)
 constexpr int kTileBytes = kBlockK * kRowBytes;
+// output staging of a finished query tile in the ring: 272-byte rows (16-byte aligned;
+// consecutive rows 4 banks apart, so 8-byte writes of 32 rows at one offset conflict 2-way)
+constexpr int kOutPitch = kRowBytes + 16;
+static_assert(kBlockQ * kOutPitch <= 2 * kStages * kTileBytes, "the output tile must fit the ring");
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr int kXcds = 8;
 
@@ -490,37 +494,51 @@ __global__ __launch_bounds__(kThreads) void window_attn_kernel(AttnArgs a) {
 
     // ---- segment epilogue: the final output, or a partial for the combine pass
     const float l_tot = acc.l + __shfl_xor(acc.l, 32);
-    if (qi < N) {
-      if (full) {
-        const float inv = 1.f / l_tot;
-        uint16_t* op = a.out + ((int64_t(b) * N + qi) * H + h) * kHeadDim + 4 * half;
+    if (full) {
+      // The tile's rows go out through the ring, free once every wave has left the walk: each
+      // lane holds 8-byte pieces of its query's row, which stored directly would make every
+      // store instruction touch 32 rows; from LDS a wave stores four whole 256-byte rows.
+      // Rows past the chunk's end are staged but not stored.
+      typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
+      typedef __attribute__((address_space(3))) bf16x4_t lds_bf16x4_t;
+      __builtin_amdgcn_s_waitcnt(0);
+      barrier();                                 // every wave has finished with the ring
+      const float inv = 1.f / l_tot;
+      const uint32_t orow = w.lds_k + uint32_t(r * kOutPitch + 8 * half);
 #pragma unroll
-        for (int d = 0; d < 4; ++d)
+      for (int d = 0; d < 4; ++d)
 #pragma unroll
-          for (int gg = 0; gg < 4; ++gg) {
-            typedef __bf16 bf16x4_t __attribute__((ext_vector_type(4)));
-            bf16x4_t rr;
+        for (int gg = 0; gg < 4; ++gg) {
+          bf16x4_t rr;
 #pragma unroll
-            for (int e = 0; e < 4; ++e) rr[e] = (__bf16)(acc.o[d][4 * gg + e] * inv);
-            *reinterpret_cast<bf16x4_t*>(op + d * 32 + 8 * gg) = rr;
-          }
-        if (a.lse && half == 0) a.lse[(int64_t(b) * H + h) * N + qi] = acc.m_off * a.scale + logf(l_tot);
-      } else {
-        const int64_t prow = (int64_t(g) * 2 + slot) * kBlockQ + r;
-        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-        float* op = a.part_o + prow * kHeadDim + 4 * half;
-#pragma unroll
-        for (int d = 0; d < 4; ++d)
-#pragma unroll
-          for (int gg = 0; gg < 4; ++gg) {
-            const float4 rr = make_float4(acc.o[d][4 * gg] * inv, acc.o[d][4 * gg + 1] * inv,
-                                          acc.o[d][4 * gg + 2] * inv, acc.o[d][4 * gg + 3] * inv);
-            *reinterpret_cast<float4*>(op + d * 32 + 8 * gg) = rr;
-          }
-        if (half == 0) {
-          a.part_ml[prow * 2] = l_tot > 0.f ? acc.m_off : -INFINITY;
-          a.part_ml[prow * 2 + 1] = l_tot;
+          for (int e = 0; e < 4; ++e) rr[e] = (__bf16)(acc.o[d][4 * gg + e] * inv);
+          *reinterpret_cast<lds_bf16x4_t*>(uintptr_t(orow + (d * 32 + 8 * gg) * 2)) = rr;
         }
+      barrier();                                 // the tile is in LDS
+      const int pc = threadIdx.x & 15;           // 16-byte piece: dims 8 pc .. 8 pc + 7
+#pragma unroll
+      for (int i = 0; i < kBlockQ / (kThreads / 16); ++i) {
+        const int rs = int(threadIdx.x >> 4) + (kThreads / 16) * i;
+        const int32_t qs = qt * kBlockQ + rs;
+        const u32x4_t v = *reinterpret_cast<const lds_u32x4_t*>(uintptr_t(w.lds_k + uint32_t(rs * kOutPitch + pc * 16)));
+        if (qs < N) *reinterpret_cast<u32x4_t*>(a.out + ((int64_t(b) * N + qs) * H + h) * kHeadDim + 8 * pc) = v;
+      }
+      if (qi < N && a.lse && half == 0) a.lse[(int64_t(b) * H + h) * N + qi] = acc.m_off * a.scale + logf(l_tot);
+    } else if (qi < N) {
+      const int64_t prow = (int64_t(g) * 2 + slot) * kBlockQ + r;
+      const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+      float* op = a.part_o + prow * kHeadDim + 4 * half;
+#pragma unroll
+      for (int d = 0; d < 4; ++d)
+#pragma unroll
+        for (int gg = 0; gg < 4; ++gg) {
+          const float4 rr = make_float4(acc.o[d][4 * gg] * inv, acc.o[d][4 * gg + 1] * inv,
+                                        acc.o[d][4 * gg + 2] * inv, acc.o[d][4 * gg + 3] * inv);
+          *reinterpret_cast<float4*>(op + d * 32 + 8 * gg) = rr;
+        }
+      if (half == 0) {
+        a.part_ml[prow * 2] = l_tot > 0.f ? acc.m_off : -INFINITY;
+        a.part_ml[prow * 2 + 1] = l_tot;
       }
     }
   }
