@@ -96,6 +96,9 @@ def parse():
                         "output in DIR (any bench mode; --trace-command is the command that made it)")
     p.add_argument("--trace-name", default=None)
     p.add_argument("--trace-command", default=None)
+    p.add_argument("--mfma-reference", action="store_true",
+                   help="time the MFMA rate reference (bf16 MFMAs alone, random operands) in the launch shapes "
+                        "of the full-frame chunk's attention and of its output projection")
     p.add_argument("--copy-calibration", type=int, default=0, metavar="MB",
                    help="only run a plain device-to-device copy of MB megabytes (x5), for scaling HBM "
                         "byte counters read by a profiler")
@@ -195,6 +198,20 @@ class Plan:
                 if need and need > self.ws.get(si, torch.empty(0)).numel():
                     self.ws[si] = torch.empty(need, dtype=torch.uint8, device=dev)
         self.step_idx = 0
+
+    def attn_launch_shape(self, f0, C, W):
+        """(work-groups, MFMAs per multiplying wave) of the attention launch of a call: one
+        work-group per 256-query tile walking all its key tiles (one M phase more than tiles),
+        or the balanced split's work-groups (from the workspace the call needs), each walking
+        about its share of the (query tile, key tile) units in up to two segments."""
+        wl = self.wl
+        qtiles = wl.B * wl.H * -(-C * wl.T // 256)
+        tk = -(-self.keys(f0, C, W) // 64)
+        need = 0 if self.no_split else self.sets[0]["cache"].workspace_bytes(f0, C, W)
+        if need == 0:
+            return qtiles, 32 * (tk + 1)
+        groups = need // (2 * 256 * 130 * 4)
+        return groups, 32 * (-(-qtiles * tk // groups) + 2)
 
     def _prefill(self, cache, randn, seed):
         wl = self.wl
@@ -836,6 +853,35 @@ def clip_bench(u, torch, args):
 SUB_WORKLOADS = ("tiny", "unwindowed", "short_refine", "rolling", "paper_default")
 
 
+def mfma_reference_us(u, torch, groups, waves_per_simd, mfmas, launches):
+    """µs per launch of unstep_mfma_reference in this shape on seeded N(0, 1) bf16 operands,
+    launched back to back (behind the device-side spin when a launch is short)."""
+    g = torch.Generator(device="cuda")
+    g.manual_seed(41)
+    src = torch.randn(groups * 512 * 128, generator=g, device="cuda").to(torch.bfloat16)
+    out = torch.empty((groups, 8), dtype=torch.float32, device="cuda")
+    ms = timed_passes(torch, lambda: u.unstep_mfma_reference(src, groups, waves_per_simd, mfmas, out=out), launches,
+                      spin=mfmas < 8192, batch=128)
+    return ms * 1e3
+
+
+def mfma_reference_bench(u, torch, args):
+    """The MFMA rate reference in the launch shapes of the full-frame chunk's attention (228
+    work-groups, two multiplying waves per SIMD, 32 MFMAs per key tile plus one M phase: 9408
+    per wave) and of its output projection (228 work-groups, one multiplying wave per SIMD, 768
+    MFMAs per wave)."""
+    steps = max(args.steps, 30)
+    shapes = {"attention_full_chunk": (228, 2, 32 * (293 + 1)), "projection_4680x1536x1536": (228, 1, 768)}
+    res = {"metric": "MFMA-only µs per launch on random bf16 operands", "unit": "us", "higher_is_better": False,
+           "launches": steps, "shapes": {}}
+    for name, (groups, wps, mfmas) in shapes.items():
+        us = mfma_reference_us(u, torch, groups, wps, mfmas, steps)
+        flops = groups * 4 * wps * mfmas * 32 * 32 * 16 * 2
+        res["shapes"][name] = {"groups": groups, "waves_per_simd": wps, "mfmas_per_wave": mfmas,
+                               "us_per_call": round(us, 2), "tflops": round(flops / (us * 1e-6) / 1e12, 1)}
+    print(json.dumps(res), flush=True)
+
+
 def measure_workload(u, torch, wl, n_sets, steps, warmup, qknorm=False, no_split=False):
     """Time `steps` whole steps of a workload after `warmup` untimed ones, then each kernel of the
     step on its own; returns the figures of one bench record (attention and append per call,
@@ -884,6 +930,15 @@ def measure_workload(u, torch, wl, n_sets, steps, warmup, qknorm=False, no_split
                                      "bytes_per_call": copy_bytes // ncalls, "gbs": round(copy_gbs, 1),
                                      "frac": round(copy_gbs / PEAK_HBM_GBS, 4),
                                      "traffic": measured_traffic("copy3_kernel", wl.name)}
+    # the MFMA work alone of this attention launch shape, on random bf16 operands (the chip's
+    # clock depends on the data): what the kernel's time compares with before the published peak
+    if wl.name != "rolling":
+        (_, f0, C, W) = plan.calls[0]
+        groups, mfmas = plan.attn_launch_shape(f0, C, W)
+        ref_us = mfma_reference_us(u, torch, groups, 2, mfmas, steps)
+        extra["mfma_reference"] = {"kernel": "mfma_reference", "groups": groups, "waves_per_simd": 2,
+                                   "mfmas_per_wave": mfmas, "us_per_call": round(ref_us, 2),
+                                   "attn_time_over_reference": round(attn_us / ref_us, 4)}
     app_kernel = "rope_norm_append_kernel" if qknorm else "rope_append_kernel"
     rec = {
         "value": round(flops / (ms * 1e-3) / 1e12, 3),
@@ -949,6 +1004,9 @@ def main():
     if args.oproj:
         oproj_bench(u, torch, args)
         return
+    if args.mfma_reference:
+        mfma_reference_bench(u, torch, args)
+        return
     headline = args.workload or "full_chunk"
     wl = synth.WORKLOADS[headline]
     m = measure_workload(u, torch, wl, args.sets, args.steps, args.warmup, qknorm=args.qknorm,
@@ -970,7 +1028,7 @@ def main():
                           "frac": m["rope_append"]["frac"],
                           "traffic": measured_traffic(app_kernel, wl.name)},
     }
-    for k in ("attn_per_chunk_us", "attn_us_per_step", "append_copy_baseline"):
+    for k in ("attn_per_chunk_us", "attn_us_per_step", "append_copy_baseline", "mfma_reference"):
         if k in m:
             res[k] = m[k]
     # every other workload of the benchmark, measured in the same run (same box, same clock

@@ -335,6 +335,22 @@ int unstep_linear(const void* x, const void* w, const void* bias, void* y, int32
 int unstep_copy3(const void* a, const void* b, const void* c, void* x, void* y, void* z, int64_t bytes,
                  void* hip_stream);
 
+/* The rate at which this chip's MFMA units run v_mfma_f32_32x32x16_bf16 on bf16 data like the
+ * method's, with no other work: `groups` work-groups of 8 waves (one per compute unit, as the
+ * attention and projection kernels launch), of which `waves_per_simd` (1: waves 0-3, 2: all 8)
+ * per SIMD multiply.  Each multiplying wave runs `mfmas` MFMAs on eight independent
+ * accumulators, its operands cycling through eight register sets loaded once from src, with a
+ * work-group barrier after every 32.  The chip is power-limited and its clock depends on how
+ * much the operand bits toggle: filled with random values of the method's magnitude, src makes
+ * the time of this launch the MFMA work alone of a kernel of that shape on such data.
+ * src: bf16 (any 16-bit pattern), device, groups * 512 * 256 bytes, lane l of work-group g
+ * reading bytes (512 g + l) * 256 .. + 255; sum: fp32, device, groups * 8 values, written with
+ * each wave's lane-0 sum of its accumulators (a checksum that keeps every MFMA).  mfmas: a
+ * positive multiple of 32.  Errors: E_NULL, E_SHAPE (groups outside [1, 65536], waves_per_simd
+ * not 1 or 2, mfmas), E_ALIGN, E_HIP. */
+int unstep_mfma_reference(const void* src, float* sum, int32_t groups, int32_t waves_per_simd, int32_t mfmas,
+                          void* hip_stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -61,6 +61,7 @@ SIGNATURES = {
     "unstep_sampler_calls": (ctypes.c_int, [_i32, _i32, _i32, _f64, _i32, _pi32, _pi32, _pi32, _pi32,
                                             ctypes.POINTER(_f64), ctypes.POINTER(_f64)]),
     "unstep_copy3": (ctypes.c_int, [_vp, _vp, _vp, _vp, _vp, _vp, _i64, _vp]),
+    "unstep_mfma_reference": (ctypes.c_int, [_vp, _vp, _i32, _i32, _i32, _vp]),
     "unstep_renoise": (ctypes.c_int, [_vp, _vp, _f64, _vp, _i64, _vp]),
     "unstep_emit": (ctypes.c_int, [_vp, _vp, _f64, _vp, _i64, _vp]),
     "unstep_window_attn": (ctypes.c_int, [_vp, _i32, _i32, _i32, _vp, _vp, _vp, _f32, _vp, _sz, _vp]),
@@ -491,3 +492,18 @@ def unstep_copy3(a: torch.Tensor, b: torch.Tensor, c: torch.Tensor, x: torch.Ten
             raise ValueError("six contiguous buffers of one size on one device")
     _check(lib.unstep_copy3(a.data_ptr(), b.data_ptr(), c.data_ptr(), x.data_ptr(), y.data_ptr(), z.data_ptr(), n,
                             _stream(stream)))
+
+
+def unstep_mfma_reference(src: torch.Tensor, groups: int, waves_per_simd: int, mfmas: int,
+                          out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    """The MFMA rate reference (not part of the method): `groups` work-groups of 8 waves,
+    `waves_per_simd` multiplying waves per SIMD, each running `mfmas` bf16 MFMAs on operands read
+    once from src (bf16, contiguous, groups * 512 * 128 values).  Returns the per-wave checksums,
+    fp32 [groups, 8]."""
+    _need(src, "src", (groups * 512 * 128,), torch.bfloat16, src.device)
+    if out is None:
+        out = torch.empty((groups, 8), dtype=torch.float32, device=src.device)
+    _need(out, "out", (groups, 8), torch.float32, src.device)
+    _check(lib.unstep_mfma_reference(src.data_ptr(), out.data_ptr(), groups, waves_per_simd, mfmas, _stream(stream)))
+    _used_on(stream, src, out)
+    return out

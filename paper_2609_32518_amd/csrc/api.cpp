@@ -484,6 +484,22 @@ int unstep_copy3(const void* a, const void* b, const void* c, void* x, void* y, 
   });
 }
 
+int unstep_mfma_reference(const void* src, float* sum, int32_t groups, int32_t waves_per_simd, int32_t mfmas,
+                          void* hip_stream) {
+  return unstep::guarded("unstep_mfma_reference", [&]() -> int {
+    const char* where = "unstep_mfma_reference";
+    if (!src || !sum) return fail(UNSTEP_E_NULL, "%s: src and sum are required", where);
+    if (groups < 1 || groups > 65536) return fail(UNSTEP_E_SHAPE, "%s: groups must be in [1, 65536]", where);
+    if (waves_per_simd != 1 && waves_per_simd != 2) return fail(UNSTEP_E_SHAPE, "%s: waves_per_simd must be 1 or 2", where);
+    if (mfmas < 32 || mfmas % 32) return fail(UNSTEP_E_SHAPE, "%s: mfmas must be a positive multiple of 32", where);
+    if (!aligned16(src) || !aligned16(sum)) return fail(UNSTEP_E_ALIGN, "%s: pointers must be 16-byte aligned", where);
+    hipError_t e = unstep::launch_mfma_reference(src, sum, groups, waves_per_simd, mfmas,
+                                                 static_cast<hipStream_t>(hip_stream));
+    if (e != hipSuccess) return fail(UNSTEP_E_HIP, "%s: %s", where, hipGetErrorString(e));
+    return ok();
+  });
+}
+
 int unstep_renoise(const void* x, const void* eps, double sigma, void* x_tilde, int64_t n, void* hip_stream) {
   return unstep::guarded("unstep_renoise", [&]() -> int {
     return flow_update("unstep_renoise", x, eps, x_tilde, n, sigma, 1.0 - sigma, sigma, hip_stream);

@@ -77,6 +77,11 @@ struct AttnPlan {
 hipError_t launch_flow_update(const uint16_t* x, const uint16_t* y, uint16_t* out, int64_t n, double a, double b,
                               hipStream_t stream);
 
+// The MFMA rate reference: `groups` work-groups of 8 waves, `waves_per_simd` (1 or 2) of each
+// SIMD's two waves running `mfmas` (a multiple of 32) bf16 MFMAs on operands from src (groups *
+// 512 lanes * 256 bytes); sum: groups * 8 floats.
+hipError_t launch_mfma_reference(const void* src, float* sum, int32_t groups, int32_t waves_per_simd,
+                                 int32_t mfmas, hipStream_t stream);
 // x = a, y = b, z = c on n16 pieces of 16 bytes each, one launch (the bandwidth reference of
 // the append pass); all pointers 16-byte aligned.
 hipError_t launch_copy3(const void* a, const void* b, const void* c, void* x, void* y, void* z, int64_t n16,

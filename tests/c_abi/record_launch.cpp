@@ -60,6 +60,7 @@ hipError_t launch_window_attn(const AttnArgs& a, hipStream_t) {
 hipError_t launch_flow_update(const uint16_t*, const uint16_t*, uint16_t*, int64_t, double, double, hipStream_t) {
   return hipSuccess;
 }
+hipError_t launch_mfma_reference(const void*, float*, int32_t, int32_t, int32_t, hipStream_t) { return hipSuccess; }
 hipError_t launch_copy3(const void*, const void*, const void*, void*, void*, void*, int64_t, hipStream_t) {
   return hipSuccess;
 }

@@ -488,6 +488,21 @@ def test_noalloc_attention_checks_arguments_before_any_device_work():
         u.lib.unstep_cache_destroy(h)
 
 
+def test_mfma_reference_argument_errors():
+    # every check runs before any device work: fake 16-byte aligned pointers are never touched
+    f = u.lib.unstep_mfma_reference
+    p = FAKE
+    assert f(None, p[1], 4, 2, 64, None) == u.E_NULL
+    assert f(p[0], None, 4, 2, 64, None) == u.E_NULL
+    assert f(p[0], p[1], 0, 2, 64, None) == u.E_SHAPE
+    assert f(p[0], p[1], 65537, 2, 64, None) == u.E_SHAPE
+    assert f(p[0], p[1], 4, 0, 64, None) == u.E_SHAPE
+    assert f(p[0], p[1], 4, 3, 64, None) == u.E_SHAPE
+    assert f(p[0], p[1], 4, 2, 0, None) == u.E_SHAPE
+    assert f(p[0], p[1], 4, 2, 48, None) == u.E_SHAPE
+    assert f(p[0] + 8, p[1], 4, 2, 64, None) == u.E_ALIGN
+
+
 def test_copy_reference_argument_errors():
     f = u.lib.unstep_copy3
     p = FAKE

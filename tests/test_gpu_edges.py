@@ -197,6 +197,51 @@ def test_snapshot_restore_through_advance():
     m.check_cache("after the restored run")
 
 
+def _mfma_reference_model(src_bits, groups, wps, mfmas):
+    """Each wave's lane-0 checksum of the MFMA rate reference, in float64: lane l of a wave holds
+    eight bf16 operand vectors a[s] and eight b[s]; a 32x32x16 MFMA takes A[i][k] from lane
+    i + 32 (k // 8), element k % 8, and B[k][j] from lane j + 32 (k // 8); block s of 32 MFMAs
+    adds A(a[(j + s) % 8]) B(b[(j // 8 + s) % 8]) into accumulator j % 8, and lane 0 holds
+    column 0, rows 0-3, 8-11, 16-19 and 24-27 of each accumulator."""
+    vals = (src_bits.astype(np.uint32) << 16).view(np.float32).astype(np.float64)
+    lanes = vals.reshape(groups, 8, 64, 16, 8)                  # group, wave, lane, vector, element
+    rows0 = [r for r in range(32) if (r // 4) % 2 == 0]
+    out = np.zeros((groups, 8))
+    for g in range(groups):
+        for w in range(4 * wps):
+            lv = lanes[g, w]
+
+            def mat(vec):                                       # [32, 16] from the 64 lanes' vector `vec`
+                return np.concatenate([lv[0:32, vec, :], lv[32:64, vec, :]], axis=1)
+            A = [mat(s) for s in range(8)]
+            Bt = [mat(8 + s) for s in range(8)]                 # Bt[j][k] = B[k][j]
+            acc = [np.zeros((32, 32)) for _ in range(8)]
+            for blk in range(mfmas // 32):
+                s = blk % 8
+                for j in range(32):
+                    acc[j % 8] += A[(j + s) % 8] @ Bt[((j // 8) + s) % 8].T
+            out[g, w] = sum(acc[i][rows0, 0].sum() for i in range(8))
+    return out
+
+
+@pytest.mark.parametrize("wps,mfmas", [(1, 64), (2, 288)])
+def test_mfma_reference_computes_its_products(wps, mfmas):
+    # the MFMA rate reference multiplies the operands it was given: per-wave checksums against a
+    # float64 model of the MFMA lane layout (288 = 9 blocks: the 8-block loop and a 1-block tail);
+    # the waves that do not multiply report zero
+    groups = 2
+    g = torch.Generator(device="cuda")
+    g.manual_seed(5)
+    src = torch.randn(groups * 512 * 128, generator=g, device="cuda").to(torch.bfloat16)
+    got = u.unstep_mfma_reference(src, groups, wps, mfmas)
+    torch.cuda.synchronize()
+    want = _mfma_reference_model(src.view(torch.int16).cpu().numpy().view(np.uint16), groups, wps, mfmas)
+    got = got.cpu().numpy().astype(np.float64)
+    assert np.all(got[:, 4 * wps:] == 0)
+    scale = np.abs(want[:, :4 * wps]).max() + 1.0
+    assert np.abs(got - want).max() <= 1e-5 * scale * mfmas, (got, want)
+
+
 def test_copy_reference_copies_bits():
     # the append pass's bandwidth reference: three buffers copied bit for bit, a ragged piece count
     n = 3 * 257 * 8 + 8                                   # 16-byte pieces, not a multiple of 256 threads
