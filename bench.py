@@ -491,7 +491,8 @@ def summarize_profile(d, workload="full_chunk", qknorm=False):
     import synth
     wl = synth.WORKLOADS[workload]
     steps = 30 * wl.layers * wl.passes        # dispatches of the timing loop: 30 steps of the workload's calls
-    for kern in ("window_attn_kernel", "rope_append_kernel<true>", "rope_norm_append_kernel<true, 3>", "copy3_kernel"):
+    for kern in ("window_attn_kernel", "rope_append_kernel<true>", "rope_norm_append_kernel<true, 3>", "copy3_kernel",
+                 "mfma_reference_kernel"):
         durs = [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in trace_rows if kname(r["Kernel_Name"]) == kern]
         if workload == "rolling" and durs:
             # the stream's bench times every call between events: its figure is the average over
