@@ -97,10 +97,11 @@ int plan_attn(const unstep_cache* c, const unstep::CacheIndex& idx, int32_t f0, 
               unstep::AttnArgs* a, const char* where) {
   if (!c) return fail(UNSTEP_E_NULL, "%s: cache handle is NULL", where);
   if (!q_rot || !out) return fail(UNSTEP_E_NULL, "%s: q_rot or out is NULL", where);
-  unstep::Segments seg;
+  unstep::Segments logical;
   std::string why;
-  int rc = idx.segments(f0, C, W, &seg, &why);
+  int rc = idx.segments(f0, C, W, &logical, &why);
   if (rc != UNSTEP_OK) return fail_msg(rc, where, why);
+  const unstep::Segments seg = unstep::cache_order(logical);
   if (!aligned16(q_rot) || !aligned16(out) || (lse && (reinterpret_cast<uintptr_t>(lse) & 3u)) ||
       (workspace && !aligned16(workspace)))
     return fail(UNSTEP_E_ALIGN, "%s: pointers must be 16-byte aligned", where);

@@ -10,6 +10,7 @@
 
 #include <cstdint>
 #include <string>
+#include <utility>
 #include <vector>
 
 #include "unstep.h"
@@ -26,6 +27,30 @@ struct Segments {
     return t;
   }
 };
+
+// The retained rows of `s` as maximal runs in ascending cache order.  Attention over the
+// retained keys does not depend on their order (every query of the chunk sees every retained
+// key, paper Section 3.3), so the attention launch walks them in cache order, where a full ring
+// and its sinks form one run however the ring has wrapped.
+inline Segments cache_order(const Segments& s) {
+  Segments o = s;
+  for (int i = 1; i < o.n; ++i)
+    for (int j = i; j > 0 && o.row0[j - 1] > o.row0[j]; --j) {
+      std::swap(o.row0[j - 1], o.row0[j]);
+      std::swap(o.len[j - 1], o.len[j]);
+    }
+  Segments m;
+  for (int i = 0; i < o.n; ++i) {
+    if (m.n > 0 && m.row0[m.n - 1] + m.len[m.n - 1] == o.row0[i]) {
+      m.len[m.n - 1] += o.len[i];
+    } else {
+      m.row0[m.n] = o.row0[i];
+      m.len[m.n] = o.len[i];
+      ++m.n;
+    }
+  }
+  return m;
+}
 
 class CacheIndex {
  public:

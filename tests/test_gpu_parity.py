@@ -154,14 +154,21 @@ def test_paper_default_sinks(u):
 # gets needle keys: raw keys drawn N(0, 40^2) at several tokens of the chunk (the end of the
 # key range), so that about one query in eight scores more than 530 on them.  Run at the
 # full-frame shape on the plain schedule (one work-group per query tile, a single run of
-# cache rows) and at the unwindowed shape on both schedules; every element against the oracle.
+# cache rows), at the unwindowed shape on both schedules, and on a wrapped window whose rows
+# form two runs (the loader's multi-run path); every element against the oracle.
+# A six-frame window at frame 27 of a twelve-frame ring: frames 21-29 sit in slots 9-11 and 0-5,
+# two runs of cache rows even in cache order, so the loader takes its multi-run path.
+WRAPPED_WINDOW = synth.Workload("wrapped_window", B=1, H=12, D=128, grid_h=30, grid_w=52, C=3, S=0, W=6, R=12,
+                                f0=27)
+
+
 @pytest.mark.parametrize("workload,use_split", [("full_chunk", False), ("unwindowed", True),
-                                                ("unwindowed", False)])
+                                                ("unwindowed", False), ("wrapped_window", False)])
 def test_exact_max_rewalk(u, workload, use_split):
-    wl = synth.WORKLOADS[workload]
+    wl = WRAPPED_WINDOW if workload == "wrapped_window" else synth.WORKLOADS[workload]
     log(f"rewalk: {workload} split={use_split}, needle keys in head 0")
     m = Mirror(u, wl.B, wl.H, wl.grid_h, wl.grid_w, wl.S, wl.R)
-    _prefill(m, wl, 17, wl.f0)
+    _prefill(m, wl, 17, wl.f0, keep_from=wl.f0 - wl.W)
     if use_split:
         assert m.lib.workspace_bytes(wl.f0, wl.C, wl.W) > 0
     key = (17, 100)
@@ -174,12 +181,14 @@ def test_exact_max_rewalk(u, workload, use_split):
     torch.cuda.synchronize()
     assert np.array_equal(host(q_rot), q_rot_ref)
     m.check_cache(f"rewalk {workload}")
+    if workload == "wrapped_window":
+        assert m.lib.segments(wl.f0, wl.C, wl.W) == [(9 * wl.T, 3 * wl.T), (0, 6 * wl.T)]
     # the construction does trigger the guard: some row of head 0 scores more than 502 raw units
-    # above the maximum of its first key tile (the range starts at logical key 0 on the plain
-    # schedule)
+    # above the maximum of its first key tile (the launch walks the retained rows in ascending
+    # cache order and, on the plain schedule, from the first of them)
     rows = m.orc.key_rows(wl.f0, wl.C, wl.W)
     qh = numerics.bf16_to_f64(q_rot_ref[0, :, 0])
-    s_first = qh @ numerics.bf16_to_f64(m.orc.k[0, 0, rows[:64]]).T
+    s_first = qh @ numerics.bf16_to_f64(m.orc.k[0, 0, np.sort(rows)[:64]]).T
     s_needle = qh @ numerics.bf16_to_f64(m.orc.k[0, 0, rows[-wl.n_query:][needles]]).T
     jump = s_needle.max(axis=1) - s_first.max(axis=1)
     log(f"  rows past the guard: {int((jump > 64 / (128 ** -0.5 * math.log2(math.e))).sum())} of {wl.n_query}")
