@@ -72,3 +72,43 @@ def test_step_replayed_from_a_graph():
         assert np.array_equal(host(q_rot), q_want)
         want, _ = a.expected(q_want, F0, C, W, query_idx=rows)
         check_attention(host(out)[:, rows], want, f"replay {r}")
+
+
+def test_noalloc_attention_replayed_from_a_graph():
+    # the allocation-free attention entry point (its split-key partials in the library's static
+    # device array) captured once and replayed with new queries written into the captured q_rot
+    # buffer between replays; each replay against the workspace entry point bit for bit and
+    # against the oracle
+    a = Mirror(u, 1, H, GH, GW, S, R)
+    _prefill(a, 62)
+    a.append(F0, C, (62, F0))
+    N = C * a.T
+    assert a.lib.workspace_bytes(F0, C, W) > 0, "this shape should take the balanced schedule"
+    shape = (1, N, H, 128)
+    q_rot = torch.zeros(shape, dtype=torch.bfloat16, device="cuda")
+    out = torch.empty(shape, dtype=torch.bfloat16, device="cuda")
+    lse = torch.empty((1, H, N), dtype=torch.float32, device="cuda")
+    # one eager call first: it looks up the static array's device address and loads the kernels,
+    # neither of which belongs in a capture
+    a.lib.unstep_window_attn_noalloc(F0, C, W, q_rot, out, lse=lse)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        a.lib.unstep_window_attn_noalloc(F0, C, W, q_rot, out, lse=lse)
+    rows = sample_queries(N, 96, 63)
+    for r in range(3):
+        log(f"noalloc graph replay {r}")
+        qb = a.inputs(C, (63, r))[0]
+        q_rot.copy_(dev(qb))
+        torch.cuda.synchronize()
+        g.replay()
+        torch.cuda.synchronize()
+        want_out = a.lib.unstep_window_attn(F0, C, W, q_rot)
+        want_lse = torch.empty_like(lse)
+        a.lib.unstep_window_attn(F0, C, W, q_rot, lse=want_lse)
+        torch.cuda.synchronize()
+        assert torch.equal(out.view(torch.int16), want_out.view(torch.int16)), f"replay {r}: output"
+        assert torch.equal(lse, want_lse), f"replay {r}: lse"
+        want, _ = a.expected(qb, F0, C, W, query_idx=rows)
+        check_attention(host(out)[:, rows], want, f"noalloc replay {r}")
+
