@@ -478,7 +478,7 @@ def summarize_profile(d, workload="full_chunk", qknorm=False):
     lines = [f"# Kernel profile — {workload} workload{' with the RMS-normalising append' if qknorm else ''}", "",
              "Commands (repo root, one MI355X, after `cd /tmp && export TMPDIR=/tmp && cd -`; DIR is an "
              "output folder; this file was written by `python bench.py --summarize-profile DIR`):", "", "```"]
-    lines += [c.replace("DIR", "gpurun_out/prof") for _, c in profile_commands(workload, qknorm)]
+    lines += [c for _, c in profile_commands(workload, qknorm)]
     lines += ["```", "", "## Kernel trace (rocprofv3 --kernel-trace --stats)", "",
               "| kernel | calls | average µs | min µs | max µs | % of GPU time |", "|---|---|---|---|---|---|"]
     for r in stats[:6]:
@@ -562,8 +562,9 @@ def summarize_trace(d, name, command):
         raise SystemExit(f"no *_kernel_stats.csv under {d}")
     stats = list(csv.DictReader(open(stats_files[0])))
     lines = [f"# Kernel profile — {name}", "",
-             "Command (repo root, one MI355X, after `cd /tmp && export TMPDIR=/tmp && cd -`; this file was "
-             "written by `python bench.py --summarize-trace DIR --trace-name NAME --trace-command CMD`):", "",
+             "Command (repo root, one MI355X, after `cd /tmp && export TMPDIR=/tmp && cd -`; DIR is an output "
+             "folder; this file was written by `python bench.py --summarize-trace DIR --trace-name NAME "
+             "--trace-command CMD`):", "",
              "```", command, "```", "", "## rocprofv3 --stats", "",
              "| kernel | calls | average µs | min µs | max µs | % of GPU time |", "|---|---|---|---|---|---|"]
     for r in stats[:8]:
@@ -616,12 +617,12 @@ def summarize_clip_profile(d, args):
     span = (int(ours[fu[-1]]["End_Timestamp"]) - int(ours[fu[0]]["Start_Timestamp"])) / 1e3
     busy = sum(sum(v) for v in groups.values())
     stats = list(csv.DictReader(open(os.path.join(d, "clip_kernel_stats.csv"))))
-    cmd = (f"rocprofv3 --kernel-trace --stats -d gpurun_out/prof_clip -o clip --output-format csv -- "
+    cmd = (f"rocprofv3 --kernel-trace --stats -d DIR -o clip --output-format csv -- "
            f"python -u bench.py --clip {variant} --clips 2 --clip-chunks {args.clip_chunks} --layers {L} "
            f"--eight-frame-layers {args.eight_frame_layers}")
     lines = [f"# Kernel profile — whole clip, {variant} sampler", "",
-             "Command (repo root, one MI355X, after `cd /tmp && export TMPDIR=/tmp && cd -`); this file was "
-             "written by `python bench.py --summarize-clip-profile gpurun_out/prof_clip` with the same clip "
+             "Command (repo root, one MI355X, after `cd /tmp && export TMPDIR=/tmp && cd -`; DIR is an output "
+             "folder); this file was written by `python bench.py --summarize-clip-profile DIR` with the same clip "
              "arguments:", "", "```", cmd, "```", "",
              f"Clip: {args.clip_chunks} chunks of {C} latent frames, {n_calls} DiT calls x {L} layers, "
              f"{H} heads x 128, {T} tokens per frame; eight-frame layers: {sorted(eight) if variant != 'self_forcing' else 'none'}.",
