@@ -19,12 +19,17 @@ max of its per-chunk attention times); --workload NAME times only that one.
 Inputs are synthetic, seeded N(0,1) bf16, resident in HBM before timing.  Several
 buffer sets (cache + inputs + outputs) are rotated so that consecutive steps do not
 find their data in the 256 MB Infinity Cache.  W warm-up steps, then K timed steps
-between device synchronisations; per-kernel durations come from HIP events recorded
-on the stream the kernels run on: each kernel of the step launched for the same calls
-back to back between two events after an untimed pass (which loads the kernels); the
-short append and copy kernels are enqueued behind a device-side spin so that the events
-bracket GPU time only, with no host enqueue gap.  A plain three-buffer copy of the append pass's inputs (unstep_copy3) is timed
-the same way as its bandwidth reference (`append_copy_baseline`).
+between device synchronisations (`value`, `ms_per_step`).  Then K more steps in which
+each call's attention (and, in the balanced schedule, its merge) sits between two HIP
+events recorded on its stream, the call enqueued as its two entry points (append, then
+attention: the kernels of unstep_step, in its order); the median over the steps of
+each call's event interval is the attention duration of `attn` and `roofline`.  Then
+each kernel of the step runs on its own for the same calls,
+back to back between two events after an untimed pass (which loads the kernels):
+the append (`rope_roofline`) and its bandwidth reference, a plain three-buffer copy of
+the append pass's inputs (unstep_copy3, `append_copy_baseline`), enqueued behind a
+device-side spin so that the events bracket GPU time only with no host enqueue gap,
+and the attention alone (`attn.us_per_call_back_to_back`).
 
 Prints one JSON line.
 """
@@ -35,6 +40,7 @@ import json
 import math
 import os
 import platform
+import statistics
 import sys
 import time
 
@@ -323,8 +329,12 @@ class Plan:
         self.step_idx = 0
         return self.behind_wait(one_step, steps, spin=True, launches_per_pass=len(self.calls))
 
-    def step(self, only=None):
-        """Enqueue one step (only="append" / "attn": just that kernel of each call)."""
+    def step(self, only=None, attn_events=None):
+        """Enqueue one step (only="append" / "attn": just that kernel of each call).  attn_events:
+        a list to which the step appends one (start, end) HIP event pair per call, recorded on the
+        current stream around that call's attention (and, in the balanced schedule, its merge);
+        the call is then enqueued as its two entry points, the append and the attention, which
+        launch the same kernels in the same order as unstep_step."""
         wl = self.wl
         if wl.name == "rolling":
             si = self.step_idx % len(self.sets)
@@ -343,6 +353,13 @@ class Plan:
                 self._append(s, f0, C, q, k, v, cos_t, sin_t, q_rot)
             elif only == "attn":
                 s["cache"].unstep_window_attn(f0, C, W, q_rot, out=out, workspace=ws, use_split=not self.no_split)
+            elif attn_events is not None:
+                self._append(s, f0, C, q, k, v, cos_t, sin_t, q_rot)
+                e0, e1 = self.torch.cuda.Event(enable_timing=True), self.torch.cuda.Event(enable_timing=True)
+                e0.record()
+                s["cache"].unstep_window_attn(f0, C, W, q_rot, out=out, workspace=ws, use_split=not self.no_split)
+                e1.record()
+                attn_events.append((e0, e1))
             elif not self.qknorm:
                 s["cache"].unstep_step(f0, C, W, q, k, v, cos_t, sin_t, q_rot=q_rot, out=out, workspace=ws,
                                        use_split=not self.no_split)
@@ -491,6 +508,15 @@ def summarize_profile(d, workload="full_chunk", qknorm=False):
     import synth
     wl = synth.WORKLOADS[workload]
     steps = 30 * wl.layers * wl.passes        # dispatches of the timing loop: 30 steps of the workload's calls
+    attn = [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in trace_rows
+            if kname(r["Kernel_Name"]) == "window_attn_kernel"]
+    if workload != "rolling" and len(attn) >= 3 * steps:
+        # the trace command runs 30 warm-up steps, 30 timed steps, then 30 steps with the attention
+        # between events: the latter's dispatches are what the bench's `attn` and `roofline` time
+        timed = attn[2 * steps:3 * steps]
+        lines.append(f"\nwindow_attn_kernel: the {steps} dispatches of the event-timed steps (the bench's `attn` "
+                     f"and `roofline` figures: median of the event intervals in the step) average "
+                     f"{sum(timed) / len(timed) / 1e3:.2f} µs, median {statistics.median(timed) / 1e3:.2f} µs.")
     for kern in ("window_attn_kernel", "rope_append_kernel<true>", "rope_norm_append_kernel<true, 3>", "copy3_kernel",
                  "mfma_reference_kernel"):
         durs = [int(r["End_Timestamp"]) - int(r["Start_Timestamp"]) for r in trace_rows if kname(r["Kernel_Name"]) == kern]
@@ -500,8 +526,9 @@ def summarize_profile(d, workload="full_chunk", qknorm=False):
             continue
         if len(durs) >= steps:
             tail = durs[-steps:]
-            lines.append(f"\n{kern}: the last {steps} dispatches (the bench's back-to-back per-kernel timing loop) "
-                         f"average {sum(tail) / len(tail) / 1e3:.2f} µs.")
+            what = "`attn.us_per_call_back_to_back`" if kern == "window_attn_kernel" else "its figure"
+            lines.append(f"\n{kern}: the last {steps} dispatches (the bench's back-to-back per-kernel timing loop, "
+                         f"{what}) average {sum(tail) / len(tail) / 1e3:.2f} µs.")
     lines += ["", "## HBM traffic per dispatch (rocprofv3 --pmc FETCH_SIZE, then WRITE_SIZE)", "",
               f"Scale factors from a plain 256 MB device copy (`--copy-calibration 256`): FETCH_SIZE read "
               f"{copy_f:.0f} KiB -> x{f_scale:.3f}; WRITE_SIZE read {copy_w:.0f} KiB -> x{w_scale:.3f}.", "",
@@ -902,19 +929,34 @@ def measure_workload(u, torch, wl, n_sets, steps, warmup, qknorm=False, no_split
     dt = time.perf_counter() - t0
     ms = dt * 1e3 / steps
 
-    # per-kernel durations: each kernel of the step launched `steps` times back to back (same
-    # calls, same rotating buffer sets) between two HIP events on the stream it runs on
+    # the same steps again with each call's attention between two HIP events on its stream, so
+    # that the attention kernel's duration is measured in the step as it runs (after the append
+    # pass, which on this power-limited chip changes the clock the attention runs at).  The
+    # events are left out of the timed steps above (each adds a short gap to the stream), and
+    # the figure is the median over the steps: a pair that brackets a moment when the host fell
+    # behind includes the idle time
+    events = []
+    for _ in range(steps):
+        plan.step(attn_events=events)
+    torch.cuda.synchronize()
+    ncalls_step = len(plan.calls)
+    in_step = [e0.elapsed_time(e1) for e0, e1 in events]
+    per_call_ms = [statistics.median(in_step[c::ncalls_step]) for c in range(ncalls_step)]
+    att_ms = sum(per_call_ms)
+
+    # then each kernel of the step on its own, launched `steps` times back to back (same calls,
+    # same rotating buffer sets) between two HIP events on the stream it runs on
     extra = {}
     if wl.name == "rolling":
         app_ms, att = plan.time_rolling(steps)
         nc = len(plan.calls)
-        att_ms = sum(att) / steps
-        per_chunk = [sum(att[s * nc + c] for s in range(steps)) * 1e3 / steps for c in range(nc)]
+        att_b2b_ms = sum(att) / steps
+        per_chunk = [x * 1e3 for x in per_call_ms]
         extra["attn_per_chunk_us"] = {"mean": round(sum(per_chunk) / nc, 2), "max": round(max(per_chunk), 2),
                                       "min": round(min(per_chunk), 2),
                                       "steady_12_frames_mean": round(sum(per_chunk[11:]) / len(per_chunk[11:]), 2)}
     else:
-        app_ms, att_ms = plan.time_kernels(steps)
+        app_ms, att_b2b_ms = plan.time_kernels(steps)
     per_call_flops = sum(attn_flops(wl.H, C * wl.T, plan.keys(f0, C, W)) * wl.B for (_, f0, C, W) in plan.calls)
     per_call_bytes = sum(plan.append_bytes(C) for (_, f0, C, W) in plan.calls)
     ncalls = len(plan.calls)
@@ -955,6 +997,7 @@ def measure_workload(u, torch, wl, n_sets, steps, warmup, qknorm=False, no_split
                    "buffer_sets": len(plan.sets)},
         "attn": {"kernel": "window_attn", "us_per_call": round(attn_us, 2), "tflops": round(attn_tflops, 2),
                  "frac": round(attn_tflops / PEAK_BF16_TFLOPS, 4),
+                 "us_per_call_back_to_back": round(att_b2b_ms * 1e3 / ncalls, 2),
                  "traffic": measured_traffic("window_attn_kernel", wl.name)},
         "rope_append": {"kernel": app_kernel[:-len("_kernel")], "us_per_call": round(app_us, 2),
                         "gbs": round(rope_gbs, 1), "frac": round(rope_gbs / PEAK_HBM_GBS, 4),
