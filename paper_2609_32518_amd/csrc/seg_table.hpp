@@ -71,6 +71,11 @@ UNSTEP_HD void cursor_at(const SegTable& seg, int32_t k_end, int32_t key, RowCur
 // keys with no lookup.  Otherwise a tile inside the cursor's run costs two compares, and only a
 // tile that crosses a run boundary or the range's end looks rows up per key and moves the
 // cursor to the run of the next tile.
+// First row of a whole tile inside the table's first run (kt0 + tile <= k_end <= l1): the tile's
+// rows are this plus 0 .. tile - 1, so the loader can put it in its scalar base and keep one
+// constant offset per lane.
+UNSTEP_HD int32_t run0_tile_row0(const SegTable& seg, int32_t kt0) { return kt0 + seg.r0; }
+
 template <bool kOneRun, int kTile, int kN, int kStride>
 UNSTEP_HD void tile_rows(const SegTable& seg, int32_t k_end, RowCursor& c, int32_t kt0, int32_t r0,
                          int32_t (&rows)[kN]) {

@@ -127,6 +127,7 @@ struct Walk {
   int lrow;                    // loader: tile row of this lane in its first load (+4 in the second)
   RowCursor kc, vc;            // loader cursors of walks over several runs (K tiles, V tiles)
   int lpiece[2];               // loader: byte offset of this lane's logical 16-byte piece
+  uint32_t loff[2];            // loader: (lrow + 4 i) rows + lpiece[i], the lane's offset in a tile
   uint32_t lds_k, lds_v;       // LDS address of ring slot 0's K tile and V tile (uniform)
   uint32_t koff[8];            // LDS address of the K fragment for d-step 0..7 in slot 0
   uint32_t voff[2][4];         // LDS address of the V^T fragment (upper 8 keys, d block) in slot 0
@@ -146,6 +147,19 @@ struct Walk {
 template <bool kOneRun>
 __device__ __forceinline__ void load_rows(uint32_t dst, const uint8_t* base, const Walk& w, RowCursor& cur, int wave,
                                           int32_t kt0) {
+  if (kOneRun && kt0 + kBlockK <= w.k_end) {
+    // a whole tile inside the single run: its first row is uniform and goes into the scalar
+    // base, each lane keeping its constant offset, so the loads need no vector address
+    // arithmetic (tile_rows' per-lane clamp to the range's last key cannot bind here)
+    const uint8_t* tb = base + int64_t(run0_tile_row0(w.seg, kt0)) * kRowBytes;
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const uint32_t off = w.loff[i];
+      const uint32_t m0 = dst + (8 * wave + 4 * i) * kRowBytes;
+      asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(tb), "{m0}"(m0) : "memory");
+    }
+    return;
+  }
   int32_t rows[2];
   tile_rows<kOneRun, kBlockK, 2, 4>(w.seg, w.k_end, cur, kt0, w.lrow, rows);
 #pragma unroll
@@ -399,7 +413,10 @@ __global__ __launch_bounds__(kThreads) void window_attn_kernel(AttnArgs a) {
   // loader: row 8 wave + 4 i + (lane >> 4); swz of that row = ((lane >> 4) << 2) | ((2 wave + i) & 3)
   w.lrow = 8 * wave + (lane >> 4);
 #pragma unroll
-  for (int i = 0; i < 2; ++i) w.lpiece[i] = ((lane & 15) ^ (((lane >> 4) << 2) | ((2 * wave + i) & 3))) * 16;
+  for (int i = 0; i < 2; ++i) {
+    w.lpiece[i] = ((lane & 15) ^ (((lane >> 4) << 2) | ((2 * wave + i) & 3))) * 16;
+    w.loff[i] = uint32_t((w.lrow + 4 * i) * kRowBytes + w.lpiece[i]);
+  }
   // K fragment for d-step st: row col (+32 kb), logical slot 2 st + half
 #pragma unroll
   for (int st = 0; st < 8; ++st) w.koff[st] = w.lds_k + col * kRowBytes + ((2 * st + half) ^ swz(col)) * 16;

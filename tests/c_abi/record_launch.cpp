@@ -135,7 +135,7 @@ std::string describe_attn(const AttnArgs& a) {
   std::vector<std::vector<int32_t>> cover(n_tiles, std::vector<int32_t>(a.n_keys, 0));
   std::vector<std::vector<int>> wrote(n_tiles);       // partial slot written by each group, per tile
   std::vector<std::vector<int64_t>> writer(n_tiles);
-  bool rows_in_bounds = true, kv_agree = true, tail_ok = true;
+  bool rows_in_bounds = true, kv_agree = true, tail_ok = true, fast_ok = true;
   int64_t segments = 0;
   for (int64_t g = 0; g < sc.G; ++g) {
     const int64_t u_begin = sc.start(g);
@@ -161,6 +161,9 @@ std::string describe_attn(const AttnArgs& a) {
             unstep::tile_rows<true, kK, kK, 1>(seg, k_end, cur, kt0, 0, rows);
           else
             unstep::tile_rows<false, kK, kK, 1>(seg, k_end, cur, kt0, 0, rows);
+          // the kernel's loader takes a whole tile inside a single run from its first row
+          if (one_run && kt0 + kK <= k_end)
+            for (int r = 0; r < kK; ++r) fast_ok = fast_ok && rows[r] == unstep::run0_tile_row0(seg, kt0) + r;
           for (int r = 0; r < kK; ++r) {
             const int32_t key = kt0 + r;
             rows_in_bounds = rows_in_bounds && rows[r] >= 0 && rows[r] < a.slots;
@@ -206,7 +209,8 @@ std::string describe_attn(const AttnArgs& a) {
                     ",\"same_rows_every_tile\":" + (same_for_all_tiles ? "true" : "false") +
                     ",\"rows_in_bounds\":" + (rows_in_bounds ? "true" : "false") +
                     ",\"tail_rows_ok\":" + (tail_ok ? "true" : "false") +
-                    ",\"merge_reads_written\":" + (merge_ok ? "true" : "false") + ",\"rows\":" + ints(rows0) + "}";
+                    ",\"merge_reads_written\":" + (merge_ok ? "true" : "false") +
+                    ",\"single_run_tiles_ok\":" + (fast_ok ? "true" : "false") + ",\"rows\":" + ints(rows0) + "}";
   return out;
 }
 

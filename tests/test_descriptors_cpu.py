@@ -113,7 +113,7 @@ class Replay:
             assert len(got["attn"]) == len(want["attn"]), where
             for a, rows in zip(got["attn"], want["attn"]):
                 for flag in ("covered_once", "k_v_agree", "same_rows_every_tile", "rows_in_bounds", "tail_rows_ok",
-                             "merge_reads_written"):
+                             "merge_reads_written", "single_run_tiles_ok"):
                     assert a[flag], (where, flag)
                 assert a["n_keys"] == len(rows), where
                 # the launch walks the retained rows in ascending cache order (attention over
