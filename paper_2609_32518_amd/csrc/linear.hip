@@ -209,6 +209,8 @@ __device__ __forceinline__ void big_load(const LinearArgs& a, uint32_t stage, in
   const uint16_t* base = is_w ? a.w + int64_t(n0) * a.K : a.x + int64_t(m0) * a.K;
   const uint32_t off = uint32_t(r) * uint32_t(a.K) * 2u + uint32_t(k0) * 2u + uint32_t(chunk) * 16u;
   const uint32_t m0addr = stage + (is_w ? 0 : kWBytes) + (is_w ? 32 * wave + 8 * j : 64 * wave + 8 * (j - 4)) * kRowBytes;
+  // `base` is computed by the scalar unit: an SGPR written by a VALU instruction would need 5 wait
+  // states before this load, which the compiler does not insert ahead of inline assembly
   asm volatile("global_load_lds_dwordx4 %0, %1" ::"v"(off), "s"(base), "{m0}"(m0addr) : "memory");
 }
 

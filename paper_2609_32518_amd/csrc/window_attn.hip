@@ -143,7 +143,9 @@ struct Walk {
 // issue slots with its softmax, which is why a range inside one run takes the lookup-free path
 // and other walks keep a cursor per operand.
 // Written as inline assembly: M0 holds the wave's LDS destination, the lane's 16 bytes land
-// at M0 + 16 l.
+// at M0 + 16 l.  The scalar base must come from the scalar unit: an SGPR that a VALU instruction
+// wrote (v_readfirstlane) needs 5 wait states before a vector-memory read of it, which the
+// compiler does not insert ahead of inline assembly.
 template <bool kOneRun>
 __device__ __forceinline__ void load_rows(uint32_t dst, const uint8_t* base, const Walk& w, RowCursor& cur, int wave,
                                           int32_t kt0) {
